@@ -1,0 +1,211 @@
+"""Seeded synthetic inputs for the batched-decode MoE layer.
+
+This module only draws random numbers and lays them out; it holds none of the
+layer's arithmetic (no gate, no selection, no bucketing, no FFN, no combine).
+Both the HIP path and the CPU oracle consume what it produces, so the two never
+disagree about an input.
+
+The paper measures the layer on real models with public datasets (Evaluation,
+"Models" and "Datasets"); none of that is available here, so every workload is
+synthetic with the model's shape:
+
+* ``tiny``            E=16,  top-2, hidden 256,  expert intermediate 128
+* ``qwen3_30b_a3b``   E=128, top-8, hidden 2048, expert intermediate 768
+* ``gpt_oss_120b``    E=128, top-4, hidden 2880, expert intermediate 2880
+
+E and top-k per model are those the paper lists (Evaluation, "Models"); hidden
+and intermediate sizes are the public model shapes.  Weights are
+N(0, 0.02) drawn in fp32 and rounded to bf16 (round-to-nearest-even, which is
+what ``torch.Tensor.to(torch.bfloat16)`` does); the gate stays fp32; hidden
+states are N(0, 1) fp32.
+
+Storage layout (row-major, "[out, in]" so each output neuron's weights are
+contiguous along the reduction axis):
+
+* gate  ``w_gate`` [E, H]  fp32
+* W1 (SwiGLU gate proj) ``w1`` [E, I, H] bf16
+* W3 (SwiGLU up proj)   ``w3`` [E, I, H] bf16
+* W2 (down proj)        ``w2`` [E, H, I] bf16
+
+Routing generators (used when the gate is bypassed) return ``ids`` [T, K]
+int32 (distinct within a token) and ``weights`` [T, K] fp32 summing to one per
+token.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+WEIGHT_STD = 0.02
+
+# Fixed child indices of SeedSequence(seed).spawn(...) so that each kind of
+# draw has its own stream, stable when other draws are added or resized.
+_STREAM_X = 0
+_STREAM_GATE = 1
+_STREAM_EXPERTS = 2
+_STREAM_ROUTING = 3
+_N_STREAMS = 8
+
+
+@dataclass(frozen=True)
+class LayerShape:
+    """Shape of one MoE layer: E experts, top-K, hidden H, expert intermediate I."""
+
+    name: str
+    E: int
+    K: int
+    H: int
+    I: int
+
+    @property
+    def expert_bytes(self) -> int:
+        """bf16 bytes of one expert's W1, W3 and W2."""
+        return 3 * self.H * self.I * 2
+
+
+SHAPES = {
+    "tiny": LayerShape("tiny", E=16, K=2, H=256, I=128),
+    "qwen3_30b_a3b": LayerShape("qwen3_30b_a3b", E=128, K=8, H=2048, I=768),
+    "gpt_oss_120b": LayerShape("gpt_oss_120b", E=128, K=4, H=2880, I=2880),
+}
+
+
+def _streams(seed: int) -> list[np.random.SeedSequence]:
+    return np.random.SeedSequence(seed).spawn(_N_STREAMS)
+
+
+def _rng(seed: int, stream: int, *extra: int) -> np.random.Generator:
+    ss = _streams(seed)[stream]
+    if extra:
+        ss = np.random.SeedSequence(ss.generate_state(4).tolist() + list(extra))
+    return np.random.default_rng(ss)
+
+
+def _torch_seed(seed: int, stream: int, *extra: int) -> int:
+    ss = _streams(seed)[stream]
+    state = np.random.SeedSequence(ss.generate_state(4).tolist() + list(extra)).generate_state(2, np.uint64)
+    return int(state[0] & np.uint64((1 << 63) - 1))
+
+
+def hidden_states(T: int, H: int, seed: int = 0, layer: int = 0) -> np.ndarray:
+    """Decode-batch hidden states x [T, H] fp32, N(0, 1)."""
+    return _rng(seed, _STREAM_X, layer).standard_normal((T, H), dtype=np.float32)
+
+
+def gate_weights(shape: LayerShape, seed: int = 0, layer: int = 0) -> np.ndarray:
+    """Gate weights stored [E, H] fp32, N(0, 0.02)."""
+    g = _rng(seed, _STREAM_GATE, layer).standard_normal((shape.E, shape.H), dtype=np.float32)
+    return (g * np.float32(WEIGHT_STD)).astype(np.float32)
+
+
+def expert_weights(shape: LayerShape, seed: int = 0, layer: int = 0, device: str = "cpu",
+                   experts: int | None = None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Expert weights (w1 [E,I,H], w3 [E,I,H], w2 [E,H,I]) as torch bf16 tensors.
+
+    Drawn with a seeded torch generator on ``device`` (fp32 N(0, 0.02), then
+    round-to-nearest-even to bf16), one expert at a time to bound the fp32
+    temporary.  The same (seed, layer, device) always yields the same bits.
+    ``experts`` limits E (used by tests that need only the first few experts).
+    """
+    E = shape.E if experts is None else experts
+    dev = torch.device(device)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(_torch_seed(seed, _STREAM_EXPERTS, layer))
+    out = []
+    for rows, cols in ((shape.I, shape.H), (shape.I, shape.H), (shape.H, shape.I)):
+        w = torch.empty((E, rows, cols), dtype=torch.bfloat16, device=dev)
+        for e in range(E):
+            tmp = torch.randn((rows, cols), generator=gen, dtype=torch.float32, device=dev)
+            w[e].copy_(tmp.mul_(WEIGHT_STD))
+        out.append(w)
+    return out[0], out[1], out[2]
+
+
+def bf16_bits(t: torch.Tensor) -> np.ndarray:
+    """Host copy of a bf16 tensor as raw uint16 bit patterns."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def dirichlet_weights(T: int, K: int, rng: np.random.Generator) -> np.ndarray:
+    """Routing weights [T, K] fp32 ~ Dirichlet(1, ..., 1) per token."""
+    return rng.dirichlet(np.ones(K), size=T).astype(np.float32)
+
+
+def controlled_routing(T: int, E: int, K: int, U: int, seed: int = 0, layer: int = 0
+                       ) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Gate-bypassed routing with a controlled expert union.
+
+    A fixed random subset of U experts is drawn once; each token then picks K
+    distinct ids uniformly from that subset, with Dirichlet(1) weights.
+    Returns (ids [T,K] int32, weights [T,K] fp32, subset [U] int32).
+    """
+    if not (1 <= K <= U <= E):
+        raise ValueError(f"need 1 <= K <= U <= E, got K={K} U={U} E={E}")
+    rng = _rng(seed, _STREAM_ROUTING, layer, U, T)
+    subset = rng.choice(E, size=U, replace=False).astype(np.int32)
+    ids = np.empty((T, K), dtype=np.int32)
+    for t in range(T):
+        ids[t] = subset[rng.choice(U, size=K, replace=False)]
+    return ids, dirichlet_weights(T, K, rng), subset
+
+
+@dataclass(frozen=True)
+class DomainModel:
+    """Domain-clustered routing: per (domain, layer) an ordered preferred subset."""
+
+    E: int = 128
+    K: int = 8
+    n_domains: int = 8
+    subset_size: int = 32
+    p_domain: float = 0.8
+    zipf_s: float = 1.1
+
+
+def domain_subsets(model: DomainModel, n_layers: int, seed: int = 0) -> np.ndarray:
+    """Preferred subsets [n_domains, n_layers, subset_size] int32 (ordered by Zipf rank)."""
+    rng = _rng(seed, _STREAM_ROUTING, 0x0D0)
+    out = np.empty((model.n_domains, n_layers, model.subset_size), dtype=np.int32)
+    for d in range(model.n_domains):
+        for layer in range(n_layers):
+            out[d, layer] = rng.choice(model.E, size=model.subset_size, replace=False)
+    return out
+
+
+def domain_routing(model: DomainModel, subsets: np.ndarray, token_domains: np.ndarray,
+                   layer: int, seed: int = 0) -> tuple[np.ndarray, np.ndarray]:
+    """One layer's routing for tokens with the given domains.
+
+    Each of a token's K picks is, with probability p_domain, the rank-r expert
+    of its domain's subset with r ~ truncated Zipf(s) over 1..subset_size, and
+    otherwise uniform over all E experts; a pick equal to one already made for
+    that token is drawn again.  Weights are Dirichlet(1).
+    """
+    T = int(token_domains.shape[0])
+    rng = _rng(seed, _STREAM_ROUTING, 0x0D1, layer, T, int(token_domains.sum()))
+    ranks = np.arange(1, model.subset_size + 1, dtype=np.float64)
+    pz = ranks ** (-model.zipf_s)
+    pz /= pz.sum()
+    ids = np.empty((T, model.K), dtype=np.int32)
+    for t in range(T):
+        sub = subsets[token_domains[t], layer]
+        chosen: list[int] = []
+        while len(chosen) < model.K:
+            if rng.random() < model.p_domain:
+                e = int(sub[rng.choice(model.subset_size, p=pz)])
+            else:
+                e = int(rng.integers(model.E))
+            if e not in chosen:
+                chosen.append(e)
+        ids[t] = chosen
+    return ids, dirichlet_weights(T, model.K, rng)
+
+
+def domain_batches(model: DomainModel, T: int, seed: int = 0) -> dict[str, np.ndarray]:
+    """Token-domain assignments for a same-domain batch per domain and an even mix."""
+    if T % model.n_domains:
+        raise ValueError("T must be a multiple of the number of domains for the mixed batch")
+    out = {f"same_{d}": np.full(T, d, dtype=np.int64) for d in range(model.n_domains)}
+    out["mixed"] = np.repeat(np.arange(model.n_domains, dtype=np.int64), T // model.n_domains)
+    return out
