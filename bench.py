@@ -1,0 +1,256 @@
+"""Benchmark of the batched-decode MoE layer on one MI355X.
+
+Default workload: one Qwen3-30B-A3B-shaped MoE layer (E=128 experts, top-8,
+hidden 2048, expert intermediate 768, SwiGLU, bf16 experts, fp32 gate), a
+decode batch of 64 tokens routed by the gate.  A step is one whole layer:
+gate scores and top-k, buckets and union, expert FFNs (up and down), combine.
+Inputs are synthetic and resident in HBM before the timed region.
+
+To keep the 256 MB Infinity Cache from serving repeated weight reads, step i
+uses weight copy i mod R, with R copies whose union bytes together exceed
+2 GB (all copies hold the same bits).
+
+Printed: one JSON line with the layer's achieved algorithmic GB/s (the
+metric), the roofline of the dominant kernel (the FFN up projection, timed
+with HIP events on the stream it runs on), and the CPU oracle's rate on the
+host cores.  ``--sweep PATH`` also writes the controlled-union and batch
+sweeps (one JSON object per point) to PATH.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2607_00466_amd import binding as B  # noqa: E402
+from paper_2607_00466_amd import synth  # noqa: E402
+
+METRIC = "MoE decode-layer µs and achieved HBM GB/s vs distinct-expert union (Qwen3-30B-A3B shape)"
+HBM_PEAK_GBS = 8000.0
+ROTATE_BYTES = 2 << 30
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def layer_bytes(shape: synth.LayerShape, T: int, U: int, gate: bool) -> int:
+    """Algorithmic HBM bytes of one layer step: the union's expert weights,
+    the gate (if routed by it), x in, out, and the routing ids and weights."""
+    b = U * shape.expert_bytes + 4 * T * shape.H * 2 + 8 * T * shape.K
+    if gate:
+        b += 4 * shape.H * shape.E
+    return b
+
+
+def up_bytes(shape: synth.LayerShape, T: int, U: int) -> int:
+    """Algorithmic bytes of one FFN up-projection launch: W1 and W3 of the union, and x."""
+    return U * 2 * shape.H * shape.I * 2 + 4 * T * shape.H
+
+
+class Bench:
+    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0):
+        self.shape = shape
+        self.T = T
+        self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        self.x_np = synth.hidden_states(T, shape.H, seed)
+        self.wg_np = synth.gate_weights(shape, seed)
+        self.x = torch.from_numpy(self.x_np).cuda()
+        self.wg = torch.from_numpy(self.wg_np).cuda()
+        self.weights = [synth.expert_weights(shape, seed, device="cuda")]
+        self.buf = B.LayerBuffers.allocate(self.d)
+        self.stream = torch.cuda.current_stream()
+
+    def rotate(self, union_bytes: int) -> None:
+        R = max(2, math.ceil(ROTATE_BYTES / max(1, union_bytes)))
+        R = min(R, 16)
+        while len(self.weights) < R:
+            self.weights.append(tuple(w.clone() for w in self.weights[0]))
+
+    def step(self, i: int, routing=None, ev=None) -> None:
+        w1, w3, w2 = self.weights[i % len(self.weights)]
+        d, b = self.d, self.buf
+        if routing is None:
+            B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
+        else:
+            b.topk_ids.copy_(routing[0])
+            b.topk_w.copy_(routing[1])
+        B.moe_bucket(b.topk_ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
+                     b.union_size)
+        if ev is not None:
+            ev[0].record(self.stream)
+        B.moe_expert_ffn_up(self.x, w1, w3, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
+                            b.ws)
+        if ev is not None:
+            ev[1].record(self.stream)
+        B.moe_expert_ffn_down(b.ws, w2, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
+                              b.y_perm)
+        if ev is not None:
+            ev[2].record(self.stream)
+        B.moe_combine(b.y_perm, b.pair_pos, b.topk_w, d, b.out)
+
+    def union(self) -> int:
+        torch.cuda.synchronize()
+        return int(self.buf.union_size.item())
+
+    def time(self, steps: int, warmup: int, routing=None) -> dict:
+        for i in range(warmup):
+            self.step(i, routing)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(self.stream)
+        for i in range(steps):
+            self.step(i, routing)
+        t1.record(self.stream)
+        torch.cuda.synchronize()
+        layer_ms = t0.elapsed_time(t1) / steps
+        # Per-kernel durations of the FFN halves, with events around each
+        # launch on the stream it runs on (a separate pass, so the events do
+        # not perturb the whole-layer timing above).
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        for i in range(steps):
+            self.step(i, routing, evs[i])
+        torch.cuda.synchronize()
+        up = np.array([e[0].elapsed_time(e[1]) for e in evs])
+        down = np.array([e[1].elapsed_time(e[2]) for e in evs])
+        return {"layer_ms": layer_ms, "up_ms": float(up.mean()), "down_ms": float(down.mean()),
+                "up_ms_median": float(np.median(up)), "down_ms_median": float(np.median(down))}
+
+
+def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:
+    """The float64 oracle on the host, one BLAS thread, on the same layer."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import moe_oracle
+
+    w1, w3, w2 = (synth.bf16_bits(w) for w in bench.weights[0])
+    runs, t_total = 0, 0.0
+    with threadpool_limits(limits=1):
+        while t_total < budget_s and runs < 50:
+            t = time.perf_counter()
+            moe_oracle.moe_layer(bench.x_np, bench.wg_np, w1, w3, w2, bench.shape.K)
+            t_total += time.perf_counter() - t
+            runs += 1
+    per_layer = t_total / runs
+    return {
+        "value": layer_bytes(bench.shape, bench.T, U, True) / per_layer / 1e9,
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{runs} runs of the whole gate-routed layer (same inputs), float64 NumPy, "
+                  f"{per_layer * 1e3:.0f} ms per layer, {os.cpu_count()} host cores visible",
+    }
+
+
+def sweep(path: str, steps: int, warmup: int) -> None:
+    """Controlled-union sweep (T=64, U in 16..128) and batch sweep (U=32, T in 8..256)."""
+    shape = synth.SHAPES["qwen3_30b_a3b"]
+    points = [(64, U) for U in (16, 32, 64, 96, 128)] + [(T, 32) for T in (8, 16, 32, 64, 128, 256)]
+    with open(path, "w") as f:
+        for T, U in points:
+            bench = Bench(shape, T)
+            ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0)
+            routing = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
+            bench.step(0, routing)
+            Ur = bench.union()
+            bench.rotate(Ur * shape.expert_bytes)
+            r = bench.time(steps, warmup, routing)
+            rec = {"T": T, "U_nominal": U, "U": Ur, "layer_us": r["layer_ms"] * 1e3,
+                   "layer_GBps": layer_bytes(shape, T, Ur, False) / r["layer_ms"] / 1e6,
+                   "up_us": r["up_ms"] * 1e3, "down_us": r["down_ms"] * 1e3,
+                   "ffn_GBps": Ur * shape.expert_bytes / (r["up_ms"] + r["down_ms"]) / 1e6}
+            rec["frac_of_peak"] = rec["layer_GBps"] / HBM_PEAK_GBS
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            log(f"sweep T={T} U={Ur}: {rec['layer_us']:.1f} us, {rec['layer_GBps']:.0f} GB/s")
+            del bench
+            torch.cuda.empty_cache()
+    # least-squares t = a + b U over the union sweep
+    recs = [json.loads(l) for l in open(path)][:5]
+    Us = np.array([r["U"] for r in recs], float)
+    ts = np.array([r["layer_us"] for r in recs], float)
+    b, a = np.polyfit(Us, ts, 1)
+    r2 = 1 - ((ts - (a + b * Us)) ** 2).sum() / ((ts - ts.mean()) ** 2).sum()
+    with open(path, "a") as f:
+        f.write(json.dumps({"fit": "layer_us = a + b * U", "a_us": a, "b_us_per_expert": b,
+                            "r2": r2, "per_expert_GBps": shape.expert_bytes / b / 1e3}) + "\n")
+    log(f"fit: t = {a:.2f} + {b:.3f} U us (R^2 {r2:.4f})")
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="host time budget of the CPU-oracle baseline (0 to skip)")
+    ap.add_argument("--sweep", default="", help="also write the union and batch sweeps to this file")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        return 2
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    B.load()
+    shape = synth.SHAPES["qwen3_30b_a3b"]
+    T = 64
+    bench = Bench(shape, T)
+    bench.step(0)
+    U = bench.union()
+    bench.rotate(U * shape.expert_bytes)
+    log(f"workload qwen3_30b_a3b T={T}: union {U}, {len(bench.weights)} weight copies")
+    r = bench.time(args.steps, args.warmup)
+    lb = layer_bytes(shape, T, U, True)
+    value = lb / r["layer_ms"] / 1e6
+    ub = up_bytes(shape, T, U)
+    achieved = ub / r["up_ms"] / 1e6
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["layer_ms"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "qwen3_30b_a3b moe layer, decode batch 64, gate-routed",
+                   "E": shape.E, "top_k": shape.K, "hidden": shape.H, "intermediate": shape.I,
+                   "tokens": T, "union": U, "weight_copies": len(bench.weights)},
+        "layer_us": round(r["layer_ms"] * 1e3, 2),
+        "layer_frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+        "ffn_up_us": round(r["up_ms"] * 1e3, 2),
+        "ffn_down_us": round(r["down_ms"] * 1e3, 2),
+        "roofline": {"bound": "hbm", "kernel": "ffn_kernel<up> (moe_expert_ffn_up)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": ub},
+    }
+    if args.cpu_seconds > 0:
+        log("timing the CPU oracle ...")
+        out["cpu_baseline"] = cpu_baseline(bench, U, args.cpu_seconds)
+    del bench
+    torch.cuda.empty_cache()
+    if args.sweep:
+        sweep(args.sweep, max(20, args.steps // 2), args.warmup)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,184 @@
+/*
+ * eldr_moe.h -- C ABI of the MI355X (gfx950) batched-decode MoE layer.
+ *
+ * The layer is the computation that ELDR's expert-locality routing speeds up
+ * (Introduction; Motivation, "Active Expert Count Drives MoE Decode Latency"):
+ * in a decode step every token is scored by the MoE gate, dispatched to its
+ * top-k experts, and the step must fetch from HBM the weights of every
+ * distinct expert the batch activates -- the union -- and nothing else.
+ * ELDR changes only which worker serves a request, so the layer itself is
+ * standard top-k gating (Introduction; Related Work) and this library computes
+ * exactly that, in four calls run back to back on one stream:
+ *
+ *   moe_gate_topk   gate scores, top-k selection and renormalised weights
+ *   moe_bucket      per-expert buckets and the distinct-expert union
+ *   moe_expert_ffn  SwiGLU FFN of every expert in the union, on its tokens
+ *   moe_combine     weighted sum of each token's k expert outputs
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every pointer argument except `stream` is a DEVICE pointer owned by the
+ *   caller; the library allocates nothing and keeps no state between calls.
+ *   `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ * - Calls are asynchronous on `stream` and never synchronise.  Device faults
+ *   surface at the caller's next synchronisation.
+ * - Return value: MOE_OK (0) after a successful launch, or a negative status
+ *   (below) when arguments are rejected before anything is launched, or
+ *   MOE_ERR_HIP when the runtime reports a launch error.  Nothing aborts,
+ *   throws or exits across this boundary.
+ * - Layouts are row-major.  Float data is IEEE binary32 ("fp32").  bf16 data
+ *   is passed as raw 16-bit patterns (uint16_t), the upper half of a binary32.
+ * - Expert weights are stored [out, in] so that each output neuron's weights
+ *   are contiguous along the reduction axis:
+ *     w_gate [E, H] fp32; w1, w3 [E, I, H] bf16; w2 [E, H, I] bf16.
+ *   The math is y = W2 (silu(W1 x) * (W3 x)) with silu(z) = z / (1 + e^-z).
+ * - Pointers to fp32 or bf16 arrays must be 16-byte aligned (the kernels use
+ *   128-bit loads and stores); int32 arrays 4-byte aligned.
+ * - T = 0 (an empty batch) is accepted everywhere: nothing is computed except
+ *   that moe_bucket still writes empty buckets and a zero union.
+ */
+#ifndef ELDR_MOE_H
+#define ELDR_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Shape of one layer invocation: T tokens, hidden size H, E experts, top-K,
+ * expert intermediate size I. */
+typedef struct moe_dims {
+  int32_t T, H, E, K, I;
+} moe_dims;
+
+/* Status codes. */
+#define MOE_OK 0
+#define MOE_ERR_INVALID (-1)     /* null pointer, negative size, K > E, ...   */
+#define MOE_ERR_UNSUPPORTED (-2) /* shape outside the limits below, bad alignment */
+#define MOE_ERR_WORKSPACE (-3)   /* workspace smaller than *_workspace_bytes  */
+#define MOE_ERR_HIP (-4)         /* the HIP runtime rejected the launch       */
+
+/* Limits.  H and I must be multiples of 32 (one MFMA reduction step). */
+#define MOE_MAX_E 256
+#define MOE_MAX_K 16
+#define MOE_MAX_T 4096
+#define MOE_MAX_H 16384
+#define MOE_MAX_I 16384
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* moe_status_string(int status);
+
+/* Version of this ABI (bumped on any incompatible change). */
+int moe_abi_version(void);
+
+/*
+ * moe_gate_topk -- the MoE gate (Introduction: the gate picks each token's
+ * experts from its hidden representation; Design, Signature Design: scores
+ * are computed for all E experts, only the discrete top-k fetch one).
+ *
+ *   logits[t, e] = sum_h x[t, h] * w_gate[e, h]        (fp32 accumulation)
+ *   topk_ids[t, :] = the K experts with the largest logits, in descending
+ *                    logit order; equal logits go to the lower expert id
+ *   topk_w[t, j]   = softmax(logits[t, :])[id] / sum over the K picks
+ *                  = exp(l_j - l_max) / sum_j' exp(l_j' - l_max)
+ *
+ * x [T, H] fp32, w_gate [E, H] fp32 (inputs).  logits [T, E] fp32,
+ * topk_ids [T, K] int32, topk_w [T, K] fp32 (outputs, all written).
+ * Every expert's score is reduced in the same order, so experts with
+ * identical gate rows tie exactly and the lower id wins.  Inputs must be
+ * finite.
+ */
+int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, float* logits,
+                  int32_t* topk_ids, float* topk_w, void* stream);
+
+/*
+ * moe_bucket -- group the batch's (token, expert) pairs by expert and form
+ * the distinct-expert union whose weights the step must load (Motivation,
+ * "Active Expert Count Drives MoE Decode Latency").
+ *
+ * topk_ids [T, K] int32 (input): ids in [0, E), distinct within a token.
+ * Outputs (all written):
+ *   counts     [E]     tokens per expert
+ *   offsets    [E+1]   exclusive prefix sum of counts; offsets[E] = T*K
+ *   perm_token [T*K]   token of each slot: experts ascending, and within an
+ *                      expert tokens ascending
+ *   pair_pos   [T*K]   pair_pos[t*K + j] = slot of (t, topk_ids[t, j])
+ *   union_ids  [E]     experts with counts > 0 ascending, then -1 padding
+ *   union_size [1]     number of distinct experts U (stays on the device)
+ * If an id is out of range or repeated within a token, union_size is set to
+ * -1 and the other outputs are unspecified; moe_expert_ffn then does nothing.
+ * Requires E * ceil(T / 32) <= 16384 (per-expert token bitmaps in LDS).
+ */
+int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* offsets,
+               int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,
+               int32_t* union_size, void* stream);
+
+/* Bytes of device workspace moe_expert_ffn needs for dims d (the SwiGLU
+ * activations of every slot, fp32 [T*K, I]).  0 when T == 0. */
+size_t moe_ffn_workspace_bytes(moe_dims d);
+
+/*
+ * moe_expert_ffn -- the expert FFNs of the union (Motivation: each step
+ * fetches the weights of every expert the batch activates; Introduction:
+ * weight reuse happens only among tokens sharing an expert).
+ *
+ * For every u < union_size, with e = union_ids[u] and its slots
+ * s in [offsets[e], offsets[e+1]) holding token t = perm_token[s]:
+ *   y_perm[s, :] = W2_e (silu(W1_e x[t]) * (W3_e x[t]))
+ * Each active expert's weights are streamed from HBM once per call when it
+ * has at most 64 tokens (a bigger bucket is processed in passes of 64 tokens,
+ * each streaming the expert's rows again); experts outside the union are
+ * never touched.
+ * The grid is sized for E experts and reads union_size on the device, so no
+ * host synchronisation is needed between moe_bucket and this call.
+ *
+ * x [T, H] fp32; w1, w3 [E, I, H] bf16; w2 [E, H, I] bf16; offsets [E+1],
+ * perm_token [T*K], union_ids [E], union_size [1] int32 (moe_bucket output).
+ * y_perm [T*K, H] fp32 output (rows of slots whose expert is not in the
+ * union are not written).  ws: device workspace of at least
+ * moe_ffn_workspace_bytes(d) bytes, 16-byte aligned, contents irrelevant.
+ * Arithmetic: bf16 weights times activations carried as a pair of bf16
+ * values (high part and rounded remainder, about 16 significant bits) on
+ * MFMA with fp32 accumulation.
+ */
+int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+                   const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,
+                   const int32_t* union_size, moe_dims d, float* y_perm, void* ws,
+                   size_t ws_bytes, void* stream);
+
+/*
+ * The two halves of moe_expert_ffn, for callers that time or schedule them
+ * separately (moe_expert_ffn is exactly up followed by down on one stream).
+ *
+ * moe_expert_ffn_up: for every slot s of an expert e in the union,
+ *   ws[s, :] = silu(W1_e x[t]) * (W3_e x[t])      (fp32 [T*K, I], t = perm_token[s])
+ * moe_expert_ffn_down: y_perm[s, :] = W2_e ws[s, :].
+ * Arguments, layouts, the workspace size and error behaviour are those of
+ * moe_expert_ffn; ws_bytes is the size of the workspace `ws`.
+ */
+int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint16_t* w3,
+                      const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,
+                      const int32_t* union_size, moe_dims d, float* ws, size_t ws_bytes,
+                      void* stream);
+int moe_expert_ffn_down(const float* ws, const uint16_t* w2, const int32_t* offsets,
+                        const int32_t* perm_token, const int32_t* union_ids,
+                        const int32_t* union_size, moe_dims d, size_t ws_bytes, float* y_perm,
+                        void* stream);
+
+/*
+ * moe_combine -- weighted unpermute: out[t, :] = sum over j = 0..K-1 (in that
+ * order) of topk_w[t, j] * y_perm[pair_pos[t*K + j], :].  Deterministic, no
+ * atomics.  y_perm [T*K, H], topk_w [T, K] fp32, pair_pos [T*K] int32
+ * (inputs); out [T, H] fp32 (output).  A pair_pos entry outside [0, T*K)
+ * contributes nothing.
+ */
+int moe_combine(const float* y_perm, const int32_t* pair_pos, const float* topk_w, moe_dims d,
+                float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ELDR_MOE_H */

@@ -1,0 +1,261 @@
+"""ctypes binding of libeldr_moe.so: argument marshalling only.
+
+Each function has the name and argument order of the C entry point it wraps
+(see include/eldr_moe.h); torch tensors stand in for device pointers and the
+stream defaults to torch's current stream.  Every step of the layer runs in
+the library's HIP kernels; there is no fallback, and a missing library or a
+non-zero status raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libeldr_moe.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "eldr_moe.h")
+
+MOE_OK = 0
+MOE_ERR_INVALID = -1
+MOE_ERR_UNSUPPORTED = -2
+MOE_ERR_WORKSPACE = -3
+MOE_ERR_HIP = -4
+
+
+class MoeDims(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("E", ctypes.c_int32),
+                ("K", ctypes.c_int32), ("I", ctypes.c_int32)]
+
+    def __repr__(self) -> str:
+        return f"MoeDims(T={self.T}, H={self.H}, E={self.E}, K={self.K}, I={self.I})"
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__(f"{fn} returned {status}: {text}")
+        self.status = status
+
+
+_vp = ctypes.c_void_p
+_SIGNATURES = {
+    "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "moe_abi_version": (ctypes.c_int, []),
+    "moe_gate_topk": (ctypes.c_int, [_vp, _vp, MoeDims, _vp, _vp, _vp, _vp]),
+    "moe_bucket": (ctypes.c_int, [_vp, MoeDims, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "moe_ffn_workspace_bytes": (ctypes.c_size_t, [MoeDims]),
+    "moe_expert_ffn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, MoeDims, _vp, _vp,
+                                      ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_up": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, MoeDims, _vp,
+                                         ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_down": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, MoeDims, ctypes.c_size_t,
+                                           _vp, _vp]),
+    "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (once); raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_00466_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def header_functions(path: str = HEADER_PATH) -> list[str]:
+    """Names of the functions include/eldr_moe.h declares."""
+    text = open(path).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(moe_\w+)\s*\(", text, re.M)))
+
+
+def status_string(status: int) -> str:
+    return load().moe_status_string(status).decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != MOE_OK:
+        raise MoeError(fn, status, status_string(status))
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, numel: int) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a device tensor, got {t.device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: needs at least {numel} elements, has {t.numel()}")
+
+
+def dims(T: int, H: int, E: int, K: int, I: int) -> MoeDims:
+    return MoeDims(T, H, E, K, I)
+
+
+# ----------------------------------------------------------------------------- entry points
+
+def moe_gate_topk(x, w_gate, d: MoeDims, logits, topk_ids, topk_w, stream=None) -> None:
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need(w_gate, "w_gate", torch.float32, d.E * d.H)
+    _need(logits, "logits", torch.float32, d.T * d.E)
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need(topk_w, "topk_w", torch.float32, d.T * d.K)
+    _check("moe_gate_topk", load().moe_gate_topk(_ptr(x), _ptr(w_gate), d, _ptr(logits),
+                                                 _ptr(topk_ids), _ptr(topk_w), _stream(stream)))
+
+
+def moe_bucket(topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos, union_ids, union_size,
+               stream=None) -> None:
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need(counts, "counts", torch.int32, d.E)
+    _need(offsets, "offsets", torch.int32, d.E + 1)
+    _need(perm_token, "perm_token", torch.int32, d.T * d.K)
+    _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
+    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_size, "union_size", torch.int32, 1)
+    _check("moe_bucket", load().moe_bucket(_ptr(topk_ids), d, _ptr(counts), _ptr(offsets),
+                                           _ptr(perm_token), _ptr(pair_pos), _ptr(union_ids),
+                                           _ptr(union_size), _stream(stream)))
+
+
+def moe_ffn_workspace_bytes(d: MoeDims) -> int:
+    return int(load().moe_ffn_workspace_bytes(d))
+
+
+def moe_expert_ffn(x, w1, w3, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
+                   ws, stream=None) -> None:
+    _need(x, "x", torch.float32, d.T * d.H)
+    for name, w, n in (("w1", w1, d.E * d.I * d.H), ("w3", w3, d.E * d.I * d.H),
+                       ("w2", w2, d.E * d.H * d.I)):
+        _need(w, name, torch.bfloat16, n)
+    _need(offsets, "offsets", torch.int32, d.E + 1)
+    _need(perm_token, "perm_token", torch.int32, d.T * d.K)
+    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_size, "union_size", torch.int32, 1)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    if ws.device.type != "cuda" or not ws.is_contiguous():
+        raise ValueError("ws: must be a contiguous device tensor")
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("moe_expert_ffn", load().moe_expert_ffn(
+        _ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(union_size), d, _ptr(y_perm), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def _need_ws(ws, d: MoeDims) -> int:
+    if ws.device.type != "cuda" or not ws.is_contiguous():
+        raise ValueError("ws: must be a contiguous device tensor")
+    return ws.numel() * ws.element_size()
+
+
+def moe_expert_ffn_up(x, w1, w3, offsets, perm_token, union_ids, union_size, d: MoeDims, ws,
+                      stream=None) -> None:
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need(w1, "w1", torch.bfloat16, d.E * d.I * d.H)
+    _need(w3, "w3", torch.bfloat16, d.E * d.I * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_up", load().moe_expert_ffn_up(
+        _ptr(x), _ptr(w1), _ptr(w3), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(union_size), d, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
+                        stream=None) -> None:
+    _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_down", load().moe_expert_ffn_down(
+        _ptr(ws), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids), _ptr(union_size), d,
+        ws_bytes, _ptr(y_perm), _stream(stream)))
+
+
+def moe_combine(y_perm, pair_pos, topk_w, d: MoeDims, out, stream=None) -> None:
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
+    _need(topk_w, "topk_w", torch.float32, d.T * d.K)
+    _need(out, "out", torch.float32, d.T * d.H)
+    _check("moe_combine", load().moe_combine(_ptr(y_perm), _ptr(pair_pos), _ptr(topk_w), d,
+                                             _ptr(out), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- a whole layer
+
+@dataclass
+class LayerBuffers:
+    """Device buffers of one layer invocation (allocated once, reused every step)."""
+
+    logits: torch.Tensor
+    topk_ids: torch.Tensor
+    topk_w: torch.Tensor
+    counts: torch.Tensor
+    offsets: torch.Tensor
+    perm_token: torch.Tensor
+    pair_pos: torch.Tensor
+    union_ids: torch.Tensor
+    union_size: torch.Tensor
+    y_perm: torch.Tensor
+    ws: torch.Tensor
+    out: torch.Tensor
+
+    @classmethod
+    def allocate(cls, d: MoeDims, device="cuda") -> "LayerBuffers":
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        nbytes = moe_ffn_workspace_bytes(d)
+        return cls(
+            logits=torch.empty((d.T, d.E), **f32),
+            topk_ids=torch.empty((d.T, d.K), **i32),
+            topk_w=torch.empty((d.T, d.K), **f32),
+            counts=torch.empty(d.E, **i32),
+            offsets=torch.empty(d.E + 1, **i32),
+            perm_token=torch.empty(max(1, d.T * d.K), **i32),
+            pair_pos=torch.empty(max(1, d.T * d.K), **i32),
+            union_ids=torch.empty(d.E, **i32),
+            union_size=torch.empty(1, **i32),
+            y_perm=torch.empty((max(1, d.T * d.K), d.H), **f32),
+            ws=torch.empty(max(16, nbytes) // 4, **f32),
+            out=torch.empty((d.T, d.H), **f32),
+        )
+
+
+def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
+    """One decode-step MoE layer: the four calls back to back on one stream.
+
+    ``routing=(topk_ids, topk_w)`` bypasses the gate (the ids are copied into
+    ``buf``).  Returns ``buf.out``.
+    """
+    if routing is None:
+        moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
+    else:
+        buf.topk_ids.copy_(routing[0])
+        buf.topk_w.copy_(routing[1])
+    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
+               buf.union_ids, buf.union_size, stream)
+    moe_expert_ffn(x, w1, w3, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
+                   buf.y_perm, buf.ws, stream)
+    moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
+    return buf.out

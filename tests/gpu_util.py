@@ -1,0 +1,135 @@
+"""Helpers for the GPU parity tests: device inputs, library calls, oracle checks."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import moe_oracle as O
+from paper_2607_00466_amd import binding as B
+from paper_2607_00466_amd import synth
+
+# Tolerances of the layer output (fp32 accumulation of bf16 weights).
+OUT_NORMWISE = 1e-2   # max |gpu - ref| / max |ref|
+OUT_MAE = 1e-3        # mean |gpu - ref|
+# With activations carried as bf16 pairs the kernels are far inside those;
+# this tighter bound catches a regression long before the stated bar does.
+OUT_NORMWISE_DESIGN = 2e-4
+WEIGHT_ATOL = 1e-5    # routing weights, absolute
+NEAR_TIE = 1e-5       # oracle logit gap below which a token's selection may differ
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+class Layer:
+    """One layer's inputs on the device, plus host copies for the oracle."""
+
+    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0, layer: int = 0,
+                 experts_on_host: bool = True):
+        self.shape = shape
+        self.T = T
+        self.x_np = synth.hidden_states(T, shape.H, seed, layer)
+        self.wg_np = synth.gate_weights(shape, seed, layer)
+        self.x = torch.from_numpy(self.x_np).cuda()
+        self.wg = torch.from_numpy(self.wg_np).cuda()
+        self.w1, self.w3, self.w2 = synth.expert_weights(shape, seed, layer, device="cuda")
+        self._host = None
+        if experts_on_host:
+            self._host = tuple(synth.bf16_bits(w) for w in (self.w1, self.w3, self.w2))
+        self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        self.buf = B.LayerBuffers.allocate(self.d)
+
+    def host_weights(self, experts=None):
+        """uint16 bit patterns of (w1, w3, w2), all experts or the listed ones (others zero)."""
+        if self._host is not None and experts is None:
+            return self._host
+        if experts is None:
+            experts = range(self.shape.E)
+        out = []
+        for w in (self.w1, self.w3, self.w2):
+            h = np.zeros((self.shape.E,) + tuple(w.shape[1:]), dtype=np.uint16)
+            for e in experts:
+                h[e] = synth.bf16_bits(w[e])
+            out.append(h)
+        return tuple(out)
+
+    def run(self, routing=None):
+        """Run the four calls; return host copies of every output."""
+        if routing is not None:
+            routing = (torch.from_numpy(np.ascontiguousarray(routing[0], np.int32)).cuda(),
+                       torch.from_numpy(np.ascontiguousarray(routing[1], np.float32)).cuda())
+        B.moe_layer(self.x, self.wg, self.w1, self.w3, self.w2, self.d, self.buf, routing=routing)
+        torch.cuda.synchronize()
+        return fetch(self.buf, self.d)
+
+
+def fetch(buf: B.LayerBuffers, d) -> dict:
+    P = d.T * d.K
+    U = int(buf.union_size.item())
+    return {
+        "logits": buf.logits.cpu().numpy(),
+        "ids": buf.topk_ids.cpu().numpy(),
+        "weights": buf.topk_w.cpu().numpy(),
+        "counts": buf.counts.cpu().numpy(),
+        "offsets": buf.offsets.cpu().numpy(),
+        "perm_token": buf.perm_token[:P].cpu().numpy(),
+        "pair_pos": buf.pair_pos[:P].cpu().numpy().reshape(d.T, d.K),
+        "union_ids": buf.union_ids.cpu().numpy(),
+        "union_size": U,
+        "y_slots": buf.y_perm[:P].cpu().numpy(),
+        "out": buf.out.cpu().numpy(),
+    }
+
+
+def compare_buckets(g: dict, ids: np.ndarray, E: int) -> None:
+    """GPU buckets and union against the oracle's on the same ids: bit-exact."""
+    r = O.bucket(ids, E)
+    for key in ("counts", "offsets", "perm_token"):
+        assert np.array_equal(g[key], r[key]), key
+    assert np.array_equal(g["pair_pos"], r["pair_pos"]), "pair_pos"
+    assert g["union_size"] == r["union_size"]
+    U = r["union_size"]
+    assert np.array_equal(g["union_ids"][:U], r["union_ids"]), "union_ids"
+    assert np.all(g["union_ids"][U:] == -1)
+
+
+def output_errors(gpu: np.ndarray, ref: np.ndarray) -> tuple[float, float]:
+    err = np.abs(gpu.astype(np.float64) - ref)
+    scale = np.abs(ref).max()
+    return float(err.max() / scale) if scale > 0 else float(err.max()), float(err.mean())
+
+
+def check_output(gpu: np.ndarray, ref: np.ndarray, label: str) -> None:
+    nw, mae = output_errors(gpu, ref)
+    say(f"  {label}: normwise max rel err {nw:.3e}, MAE {mae:.3e}")
+    assert nw <= OUT_NORMWISE and mae <= OUT_MAE, label
+    assert nw <= OUT_NORMWISE_DESIGN, f"{label}: above the split-bf16 design bound"
+
+
+def check_gate(g: dict, x_np, wg_np, K: int) -> np.ndarray:
+    """Gate stage vs oracle; returns the mask of near-tie tokens (exempt from id equality)."""
+    logits = O.gate_logits(x_np, wg_np)
+    scale = np.abs(logits).max()
+    assert np.abs(g["logits"] - logits).max() <= 1e-5 * max(1.0, scale), "logits"
+    gaps = O.selection_gaps(logits, K)
+    near = gaps < NEAR_TIE
+    for t in np.nonzero(near)[0]:
+        say(f"  near-tie: token {t} gap {gaps[t]:.3e} oracle "
+            f"{sorted(O.select_experts(logits[t:t+1], K)[0].tolist())} gpu {sorted(g['ids'][t].tolist())}")
+    ref_ids = O.select_experts(logits, K)
+    ok = ~near
+    assert np.array_equal(np.sort(g["ids"][ok], 1), np.sort(ref_ids[ok], 1)), "top-k sets"
+    # weights, matched by id, against the oracle on the GPU's own selection
+    w_ref = O.routing_weights(logits, g["ids"].astype(np.int64))
+    assert np.abs(g["weights"] - w_ref).max() <= WEIGHT_ATOL, "weights"
+    assert np.abs(g["weights"].sum(1) - 1.0).max() <= 1e-6, "weights sum"
+    # order: descending logit, ties to the lower id (checked on the GPU logits)
+    for t in range(g["ids"].shape[0]):
+        lt = g["logits"][t, g["ids"][t]]
+        for j in range(K - 1):
+            assert lt[j] > lt[j + 1] or (lt[j] == lt[j + 1] and g["ids"][t, j] < g["ids"][t, j + 1])
+    return near

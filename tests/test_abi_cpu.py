@@ -1,0 +1,108 @@
+"""The C-ABI library loads, exports what its header declares, and rejects bad
+arguments on the host before anything is launched (no GPU needed)."""
+import ctypes
+
+import pytest
+
+from paper_2607_00466_amd import binding as B
+
+FAKE = ctypes.c_void_p(0x10000)        # 16-byte aligned, never dereferenced
+FAKE_MIS = ctypes.c_void_p(0x10004)    # 4-byte aligned only
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load()
+
+
+def test_exports_every_declared_function(lib):
+    names = B.header_functions()
+    assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_combine",
+            "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    assert lib.moe_abi_version() == 1
+    for st in (B.MOE_OK, B.MOE_ERR_INVALID, B.MOE_ERR_UNSUPPORTED, B.MOE_ERR_WORKSPACE, B.MOE_ERR_HIP):
+        assert B.status_string(st).startswith("MOE_")
+    assert B.status_string(12345) == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    assert B.moe_ffn_workspace_bytes(B.dims(64, 2048, 128, 8, 768)) == 64 * 8 * 768 * 4
+    assert B.moe_ffn_workspace_bytes(B.dims(0, 2048, 128, 8, 768)) == 0
+    assert B.moe_ffn_workspace_bytes(B.dims(8, 2048, 4, 8, 768)) == 0  # K > E is invalid
+
+
+GOOD = (64, 2048, 128, 8, 768)
+
+
+@pytest.mark.parametrize("dims,status", [
+    ((64, 2048, 128, 129, 768), B.MOE_ERR_INVALID),      # K > E
+    ((-1, 2048, 128, 8, 768), B.MOE_ERR_INVALID),        # negative T
+    ((64, 0, 128, 8, 768), B.MOE_ERR_INVALID),           # H = 0
+    ((64, 2048, 257, 8, 768), B.MOE_ERR_UNSUPPORTED),    # E above the limit
+    ((64, 2048, 128, 17, 768), B.MOE_ERR_UNSUPPORTED),   # K above the limit
+    ((4097, 2048, 128, 8, 768), B.MOE_ERR_UNSUPPORTED),  # T above the limit
+    ((64, 2040, 128, 8, 768), B.MOE_ERR_UNSUPPORTED),    # H not a multiple of 32
+    ((64, 2048, 128, 8, 760), B.MOE_ERR_UNSUPPORTED),    # I not a multiple of 32
+])
+def test_dims_rejected_by_every_call(lib, dims, status):
+    d = B.dims(*dims)
+    s = None
+    assert lib.moe_gate_topk(FAKE, FAKE, d, FAKE, FAKE, FAKE, s) == status
+    assert lib.moe_bucket(FAKE, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, s) == status
+    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+                              1 << 40, s) == status
+    assert lib.moe_combine(FAKE, FAKE, FAKE, d, FAKE, s) == status
+
+
+def test_null_pointers_rejected(lib):
+    d = B.dims(*GOOD)
+    assert lib.moe_gate_topk(None, FAKE, d, FAKE, FAKE, FAKE, None) == B.MOE_ERR_INVALID
+    assert lib.moe_bucket(FAKE, d, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.MOE_ERR_INVALID
+    assert lib.moe_expert_ffn(FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+                              1 << 40, None) == B.MOE_ERR_INVALID
+    assert lib.moe_combine(FAKE, FAKE, FAKE, d, None, None) == B.MOE_ERR_INVALID
+
+
+def test_misaligned_pointers_rejected(lib):
+    d = B.dims(*GOOD)
+    assert lib.moe_gate_topk(FAKE_MIS, FAKE, d, FAKE, FAKE, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+    assert lib.moe_expert_ffn(FAKE, FAKE_MIS, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+                              1 << 40, None) == B.MOE_ERR_UNSUPPORTED
+    assert lib.moe_combine(FAKE_MIS, FAKE, FAKE, d, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+    odd = ctypes.c_void_p(0x10002)
+    assert lib.moe_bucket(odd, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+
+
+def test_workspace_too_small_rejected(lib):
+    d = B.dims(*GOOD)
+    need = B.moe_ffn_workspace_bytes(d)
+    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+                              need - 1, None) == B.MOE_ERR_WORKSPACE
+
+
+def test_bucket_bitmap_limit(lib):
+    # E * ceil(T / 32) must stay within 16384 words of LDS bitmaps.
+    d = B.dims(4096, 2048, 256, 8, 768)
+    assert lib.moe_bucket(FAKE, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+
+
+def test_empty_batch_is_a_no_op(lib):
+    # T = 0: gate, ffn and combine return before any launch.
+    d = B.dims(0, 2048, 128, 8, 768)
+    assert lib.moe_gate_topk(None, None, d, None, None, None, None) == B.MOE_OK
+    assert lib.moe_expert_ffn(None, None, None, None, None, None, None, None, d, None, None, 0,
+                              None) == B.MOE_OK
+    assert lib.moe_combine(None, None, None, d, None, None) == B.MOE_OK
+
+
+def test_binding_requires_device_tensors():
+    import torch
+    d = B.dims(2, 64, 4, 2, 32)
+    with pytest.raises(ValueError):
+        B.moe_combine(torch.zeros(4, 64), torch.zeros(4, dtype=torch.int32), torch.zeros(2, 2), d,
+                      torch.zeros(2, 64))

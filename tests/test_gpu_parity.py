@@ -1,0 +1,227 @@
+"""GPU parity: every stage of the HIP path against the CPU oracle.
+
+Each stage is compared with the oracle stage run on the GPU's own upstream
+output (ids for the buckets, buckets for the FFN), so integer outputs are
+compared bit-exactly even when a near-tie (logit gap < 1e-5) lets the GPU
+pick a different expert; the end-to-end output is compared only for tokens
+whose selection is not a near-tie.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2607_00466_amd import binding as B
+from paper_2607_00466_amd import synth
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.SHAPES["tiny"]
+QWEN = synth.SHAPES["qwen3_30b_a3b"]
+GPTOSS = synth.SHAPES["gpt_oss_120b"]
+
+
+@pytest.fixture(scope="module")
+def qwen_layer():
+    G.say("building the qwen3_30b_a3b-shaped layer (E=128 top-8 H=2048 I=768), T=64")
+    return G.Layer(QWEN, 64)
+
+
+def _full_check(layer: G.Layer, g: dict, routed_by_gate: bool, routing=None) -> None:
+    s = layer.shape
+    w1, w3, w2 = layer.host_weights()
+    if routed_by_gate:
+        near = G.check_gate(g, layer.x_np, layer.wg_np, s.K)
+        ids, wts = g["ids"].astype(np.int64), g["weights"]
+    else:
+        near = np.zeros(layer.T, dtype=bool)
+        ids, wts = routing
+    G.compare_buckets(g, ids, s.E)
+    b = O.bucket(ids, s.E)
+    y = O.expert_ffn(layer.x_np, w1, w3, w2, ids, b)
+    G.check_output(g["y_slots"], y, "expert FFN per slot")
+    out = O.combine(y, b["pair_pos"], np.asarray(wts, np.float64))
+    G.check_output(g["out"], out, "layer output (GPU routing)")
+    if routed_by_gate:
+        ref = O.moe_layer(layer.x_np, layer.wg_np, w1, w3, w2, s.K)
+        ok = ~near
+        G.check_output(g["out"][ok], ref["out"][ok], "layer output vs oracle end to end")
+
+
+def test_tiny_layer_end_to_end():
+    G.say("case: tiny layer E=16 top-2 H=256 I=128 T=8 seed 0, gate-routed")
+    layer = G.Layer(TINY, 8)
+    g = layer.run()
+    _full_check(layer, g, True)
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_tiny_layer_seeds(seed):
+    G.say(f"case: tiny layer seed {seed}, T=40 (ragged token tiles)")
+    layer = G.Layer(TINY, 40, seed=seed)
+    _full_check(layer, layer.run(), True)
+
+
+def test_qwen_layer_gate_routed(qwen_layer):
+    G.say("case: qwen layer gate-routed T=64")
+    g = qwen_layer.run()
+    G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
+    _full_check(qwen_layer, g, True)
+
+
+@pytest.mark.parametrize("U", [16, 32, 64, 96, 128])
+def test_qwen_controlled_union(qwen_layer, U):
+    G.say(f"case: qwen layer, gate bypassed, controlled union U={U}, T=64")
+    ids, w, _ = synth.controlled_routing(64, QWEN.E, QWEN.K, U, seed=0)
+    g = qwen_layer.run(routing=(ids, w))
+    assert g["union_size"] == len(set(ids.ravel().tolist()))
+    _full_check(qwen_layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+@pytest.mark.parametrize("T", [1, 8, 16, 17, 128, 256])
+def test_qwen_batch_sweep(T):
+    G.say(f"case: qwen layer, controlled union U=32, batch T={T}")
+    layer = G.Layer(QWEN, T)
+    ids, w, _ = synth.controlled_routing(T, QWEN.E, QWEN.K, 32, seed=T)
+    g = layer.run(routing=(ids, w))
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+def test_bucket_over_64_tokens_takes_passes():
+    # Every token picks the same 8 experts: 200 tokens per bucket, four passes.
+    G.say("case: qwen layer, T=200, all tokens on experts 0..7 (buckets of 200)")
+    layer = G.Layer(QWEN, 200)
+    ids = np.tile(np.arange(8, dtype=np.int32), (200, 1))
+    w = np.full((200, 8), 1 / 8, np.float32)
+    g = layer.run(routing=(ids, w))
+    assert g["union_size"] == 8
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+def test_ragged_shape_partial_bands():
+    # H and I multiples of 32 but not of the 64/128-row bands; E not a multiple of 8.
+    G.say("case: ragged shape E=13 top-3 H=352 I=96 T=21")
+    shape = synth.LayerShape("ragged", E=13, K=3, H=352, I=96)
+    layer = G.Layer(shape, 21, seed=4)
+    _full_check(layer, layer.run(), True)
+
+
+def test_k_equals_e():
+    G.say("case: K = E = 16, H=256 I=128 T=5")
+    shape = synth.LayerShape("k_eq_e", E=16, K=16, H=256, I=128)
+    layer = G.Layer(shape, 5, seed=6)
+    g = layer.run()
+    assert g["union_size"] == 16
+    _full_check(layer, g, True)
+
+
+def test_duplicate_gate_rows_tie_to_lower_id():
+    G.say("case: gate rows 3 and 11 identical (exact ties), tiny shape T=64")
+    layer = G.Layer(TINY, 64, seed=9)
+    layer.wg_np = layer.wg_np.copy()
+    layer.wg_np[11] = layer.wg_np[3]
+    layer.wg = torch.from_numpy(layer.wg_np).cuda()
+    g = layer.run()
+    assert np.array_equal(g["logits"][:, 3], g["logits"][:, 11])
+    for row in g["ids"].tolist():
+        if 11 in row:
+            assert 3 in row and row.index(3) < row.index(11)
+    assert any(3 in row and 11 not in row for row in g["ids"].tolist())
+    _full_check(layer, g, True)
+
+
+def test_zero_input():
+    G.say("case: x = 0 (all logits 0): ids 0..K-1, weights 1/K, output 0")
+    layer = G.Layer(TINY, 8)
+    layer.x.zero_()
+    layer.x_np = np.zeros_like(layer.x_np)
+    g = layer.run()
+    assert np.array_equal(g["ids"], np.tile(np.arange(TINY.K), (8, 1)))
+    assert np.all(g["weights"] == np.float32(1.0 / TINY.K))
+    assert np.all(g["out"] == 0)
+
+
+def test_empty_batch():
+    G.say("case: T = 0")
+    d = B.dims(0, TINY.H, TINY.E, TINY.K, TINY.I)
+    buf = B.LayerBuffers.allocate(d)
+    buf.union_size.fill_(77)
+    buf.counts.fill_(5)
+    x = torch.empty((0, TINY.H), device="cuda")
+    w1, w3, w2 = synth.expert_weights(TINY, device="cuda")
+    B.moe_layer(x, torch.zeros((TINY.E, TINY.H), device="cuda"), w1, w3, w2, d, buf)
+    torch.cuda.synchronize()
+    assert int(buf.union_size.item()) == 0
+    assert int(buf.counts.abs().sum().item()) == 0
+    assert int(buf.offsets.abs().sum().item()) == 0
+    assert bool((buf.union_ids == -1).all())
+
+
+def test_invalid_routing_flags_union():
+    G.say("case: repeated id within a token -> union_size = -1, FFN does nothing")
+    layer = G.Layer(TINY, 4)
+    ids = np.array([[1, 1], [2, 3], [4, 5], [6, 7]], np.int32)
+    w = np.full((4, 2), 0.5, np.float32)
+    layer.buf.y_perm.fill_(123.0)
+    g = layer.run(routing=(ids, w))
+    assert g["union_size"] == -1
+    assert np.all(g["y_slots"] == 123.0)
+    ids2 = np.array([[1, 16], [2, 3], [4, 5], [6, 7]], np.int32)  # out of range
+    g = layer.run(routing=(ids2, w))
+    assert g["union_size"] == -1
+
+
+def test_bucket_large_batch():
+    G.say("case: bucket only, T=4096 E=128 K=8 (bitmap limit)")
+    T, E, K = 4096, 128, 8
+    rng = np.random.default_rng(5)
+    ids = np.stack([rng.choice(E, K, replace=False) for _ in range(T)]).astype(np.int32)
+    d = B.dims(T, 64, E, K, 32)
+    buf = B.LayerBuffers.allocate(d)
+    B.moe_bucket(torch.from_numpy(ids).cuda(), d, buf.counts, buf.offsets, buf.perm_token,
+                 buf.pair_pos, buf.union_ids, buf.union_size)
+    torch.cuda.synchronize()
+    G.compare_buckets(G.fetch(buf, d), ids.astype(np.int64), E)
+
+
+def test_combine_alone():
+    G.say("case: combine on oracle slot outputs, qwen shape T=64")
+    T, E, K, H = 64, 128, 8, 2048
+    ids, w, _ = synth.controlled_routing(T, E, K, 48, seed=3)
+    b = O.bucket(ids.astype(np.int64), E)
+    rng = np.random.default_rng(8)
+    y = rng.standard_normal((T * K, H)).astype(np.float32)
+    d = B.dims(T, H, E, K, 768)
+    out = torch.empty((T, H), device="cuda")
+    B.moe_combine(torch.from_numpy(y).cuda(), torch.from_numpy(b["pair_pos"].ravel().astype(np.int32)).cuda(),
+                  torch.from_numpy(w).cuda(), d, out)
+    torch.cuda.synchronize()
+    ref = O.combine(y.astype(np.float64), b["pair_pos"], w.astype(np.float64))
+    assert np.abs(out.cpu().numpy() - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
+def test_deterministic(qwen_layer):
+    G.say("case: two runs of the qwen layer are bitwise equal")
+    a = qwen_layer.run()
+    b = qwen_layer.run()
+    for key in ("logits", "ids", "weights", "counts", "offsets", "perm_token", "pair_pos",
+                "union_ids", "y_slots", "out"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_gpt_oss_layer_sampled():
+    # Full gpt-oss shape (6.4 GB of bf16 experts); the oracle checks a sample of tokens.
+    G.say("case: gpt-oss-shaped layer E=128 top-4 H=I=2880 T=256, gate-routed, sampled tokens")
+    layer = G.Layer(GPTOSS, 256, experts_on_host=False)
+    g = layer.run()
+    G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
+    near = G.check_gate(g, layer.x_np, layer.wg_np, GPTOSS.K)
+    ids = g["ids"].astype(np.int64)
+    G.compare_buckets(g, ids, GPTOSS.E)
+    sample = [t for t in (0, 1, 77, 128, 200, 255) if not near[t]]
+    experts = sorted(set(ids[sample].ravel().tolist()))
+    w1, w3, w2 = layer.host_weights(experts)
+    sub = O.moe_layer_routed(layer.x_np[sample], ids[sample], g["weights"][sample].astype(np.float64),
+                             w1, w3, w2, GPTOSS.E)
+    G.check_output(g["out"][sample], sub["out"], "sampled tokens")
