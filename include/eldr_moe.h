@@ -115,8 +115,9 @@ int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* of
                int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,
                int32_t* union_size, void* stream);
 
-/* Bytes of device workspace moe_expert_ffn needs for dims d (the SwiGLU
- * activations of every slot, fp32 [T*K, I]).  0 when T == 0. */
+/* Bytes of device workspace moe_expert_ffn needs for dims d: the SwiGLU
+ * activations of every slot and a copy of x, each stored as pairs of bf16
+ * values (4 bytes a value): 4 * (T*K*I + T*H).  0 when T == 0. */
 size_t moe_ffn_workspace_bytes(moe_dims d);
 
 /*
@@ -152,17 +153,19 @@ int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t* w3, const
  * The two halves of moe_expert_ffn, for callers that time or schedule them
  * separately (moe_expert_ffn is exactly up followed by down on one stream).
  *
- * moe_expert_ffn_up: for every slot s of an expert e in the union,
- *   ws[s, :] = silu(W1_e x[t]) * (W3_e x[t])      (fp32 [T*K, I], t = perm_token[s])
- * moe_expert_ffn_down: y_perm[s, :] = W2_e ws[s, :].
+ * moe_expert_ffn_up: for every slot s of an expert e in the union, the
+ *   activation h_s = silu(W1_e x[t]) * (W3_e x[t]), t = perm_token[s], is
+ *   left in the workspace (as a pair of bf16 values per element).
+ * moe_expert_ffn_down: y_perm[s, :] = W2_e h_s, reading h from the workspace.
  * Arguments, layouts, the workspace size and error behaviour are those of
- * moe_expert_ffn; ws_bytes is the size of the workspace `ws`.
+ * moe_expert_ffn; ws_bytes is the size of the workspace `ws`, which must be
+ * the one the preceding moe_expert_ffn_up call filled.
  */
 int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint16_t* w3,
                       const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,
-                      const int32_t* union_size, moe_dims d, float* ws, size_t ws_bytes,
+                      const int32_t* union_size, moe_dims d, void* ws, size_t ws_bytes,
                       void* stream);
-int moe_expert_ffn_down(const float* ws, const uint16_t* w2, const int32_t* offsets,
+int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offsets,
                         const int32_t* perm_token, const int32_t* union_ids,
                         const int32_t* union_size, moe_dims d, size_t ws_bytes, float* y_perm,
                         void* stream);

@@ -13,6 +13,9 @@ constexpr int kNumXcd = 8;   // MI355X: 8 XCDs, workgroups dispatched round-robi
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+// Native 128-bit vector (HIP's uint4 is a struct the optimiser cannot always
+// keep in registers when it is copied whole).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // fp32 -> bf16 bit pattern, round to nearest even (inputs are finite; a NaN
 // keeps a quiet-NaN pattern).
@@ -32,13 +35,13 @@ __device__ __forceinline__ void split_bf16(float v, uint32_t& hi, uint32_t& lo) 
   lo = f32_to_bf16_bits(v - bf16_bits_to_f32(hi));
 }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // 16x16x32 bf16 MFMA with fp32 accumulation.  A lane supplies 8 k-values of
 // one row of A (row = lane % 16) and 8 k-values of one column of B
 // (column = lane % 16), the k-set chosen by lane / 16 identically for A and
 // B; the result lane holds D[4 * (lane / 16) + i][lane % 16], i = 0..3.
-__device__ __forceinline__ f32x4 mfma16x16x32(uint4 a, uint4 b, f32x4 c) {
+__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 

@@ -25,30 +25,46 @@
 
 namespace eldr {
 
+#ifndef ELDR_FFN_RING_SMALL
+#define ELDR_FFN_RING_SMALL 4
+#endif
+#ifndef ELDR_FFN_RING_LARGE
+#define ELDR_FFN_RING_LARGE 4
+#endif
+
 constexpr int kFfnThreads = 256;  // 4 waves
 constexpr int kFfnWaves = kFfnThreads / kWave;
 constexpr int kKStep = 32;        // k per MFMA
-constexpr int kRing = 4;          // k-steps of weights in flight per wave (prefetch depth)
 constexpr int kMaxTiles = 4;      // token tiles of 16 per pass: at most 64 tokens per pass
 
-// Bytes of one LDS staging buffer (two are used, double-buffered).  Large
-// enough that a chunk of kRing k-steps fits for the largest pass.
+// k-steps of weights in flight per wave (the prefetch depth of the ring).
+template <int NT>
+__host__ __device__ constexpr int ring_depth() {
+  return NT <= 2 ? ELDR_FFN_RING_SMALL : ELDR_FFN_RING_LARGE;
+}
+
+// Bytes of one LDS staging buffer (two are used, double-buffered): at least
+// a base size, and always room for a chunk of ring_depth k-steps of the
+// largest pass (NT * 16 tokens, 128 bytes per k-step, 16 bytes of padding).
 template <int NT>
 __host__ __device__ constexpr int lds_buf_bytes() {
-  return NT == 1 ? 16 * 1024 : NT == 2 ? 24 * 1024 : 34 * 1024;
+  constexpr int base = NT == 1 ? 16 * 1024 : NT == 2 ? 24 * 1024 : 34 * 1024;
+  constexpr int need = NT * 16 * (128 * ring_depth<NT>() + 16);
+  return base > need ? base : ((need + 1023) / 1024) * 1024;
 }
 
 enum FfnMode { kUp = 0, kDown = 1 };
 
 struct FfnArgs {
-  const float* src;            // up: x [T, H]; down: h workspace [T*K, I]
+  const uint4* src;            // activations as bf16 pairs (see split_rows_kernel):
+                               // up: x [T, H]; down: h [T*K, I]
   const uint16_t* wa;          // up: W1 [E, I, H]; down: W2 [E, H, I]
   const uint16_t* wb;          // up: W3 [E, I, H]; down: unused
   const int32_t* offsets;      // [E+1]
   const int32_t* perm_token;   // [T*K]
   const int32_t* union_ids;    // [E]
   const int32_t* union_size;   // [1]
-  float* dst;                  // up: h workspace [T*K, I]; down: y_perm [T*K, H]
+  void* dst;                   // up: h [T*K, I] as bf16 pairs; down: y_perm [T*K, H] fp32
   int rows;                    // output rows per expert: up I, down H
   int kdim;                    // reduction length: up H, down I
   int tiles;                   // workgroups per expert
@@ -67,6 +83,20 @@ __host__ __device__ constexpr int rows_per_block() {
 // multiple of 16, so the 16 lanes that read 16 tokens hit distinct banks.
 __device__ __forceinline__ int lds_stride(int kcs) { return 128 * kcs + 16; }
 
+template <int N>
+struct Int {
+  static constexpr int value = N;
+};
+
+// Calls f(Int<0>{}), ..., f(Int<N-1>{}) -- a loop whose index is a constant.
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(Int<I>{});
+    static_for<N, F, I + 1>(static_cast<F&&>(f));
+  }
+}
+
 // Pack 8 fp32 values as 8 bf16 high parts and 8 bf16 low parts.
 __device__ __forceinline__ void split8(const float4& a, const float4& b, uint4& hi, uint4& lo) {
   const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
@@ -77,9 +107,27 @@ __device__ __forceinline__ void split8(const float4& a, const float4& b, uint4& 
   lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
 }
 
+// Activations enter the MFMA B operand as a pair of bf16 numbers (high
+// part, rounded remainder).  In memory a row of K values is K / 8 groups of
+// 32 bytes: 8 bf16 high parts, then the 8 matching low parts -- the same
+// 4 bytes per value as fp32, and exactly the layout staged in LDS, so that
+// staging is a plain copy.  This kernel writes x in that form, one group per
+// thread.
+__global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict__ src, int ngroups,
+                                                         uint4* __restrict__ dst) {
+  const int g = blockIdx.x * 256 + threadIdx.x;
+  if (g >= ngroups) return;
+  const float4* p = reinterpret_cast<const float4*>(src) + 2 * (size_t)g;
+  uint4 hi, lo;
+  split8(p[0], p[1], hi, lo);
+  dst[2 * (size_t)g] = hi;
+  dst[2 * (size_t)g + 1] = lo;
+}
+
 template <int MODE, int NT>
 __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   constexpr int kBuf = lds_buf_bytes<NT>();
+  constexpr int kRing = ring_depth<NT>();
   static_assert(kBuf >= NT * 16 * (128 * kRing + 16), "a chunk of kRing k-steps must fit");
   constexpr int kGroups = (kBuf / 32 + kFfnThreads - 1) / kFfnThreads;  // staged groups per thread
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
@@ -131,22 +179,25 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
     if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
     __syncthreads();
 
-    // Fetch this thread's share of chunk [ks, ks + klen) k-steps into registers.
-    float4 stg[kGroups][2];
+    // Fetch this thread's share of chunk [ks, ks + klen) k-steps into
+    // registers.  Every thread issues the same loads (a thread with no group
+    // left re-reads group 0), so the number of loads in flight is the same on
+    // every path and the compiler never has to drain the weight ring.
+    const size_t row_groups = (size_t)K / 8;  // 32-byte groups per activation row
+    u32x4 stg[kGroups][2];
     auto fetch = [&](int ks, int klen) {
       const int gpr = 4 * klen;
       const int ng = c * gpr;
 #pragma unroll
       for (int j = 0; j < kGroups; ++j) {
-        const int q = tid + kFfnThreads * j;
-        if (q < ng) {
-          const int n = q / gpr;
-          const int gi = q - n * gpr;
-          const float4* p =
-              reinterpret_cast<const float4*>(a.src + (size_t)tok[n] * K + ks * kKStep + gi * 8);
-          stg[j][0] = p[0];
-          stg[j][1] = p[1];
-        }
+        int q = tid + kFfnThreads * j;
+        q = q < ng ? q : 0;
+        const int n = q / gpr;
+        const int gi = q - n * gpr;
+        const u32x4* p =
+            reinterpret_cast<const u32x4*>(a.src) + 2 * ((size_t)tok[n] * row_groups + ks * 4 + gi);
+        stg[j][0] = p[0];
+        stg[j][1] = p[1];
       }
     };
     auto publish = [&](int buf, int klen) {
@@ -158,11 +209,9 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
         if (q < ng) {
           const int n = q / gpr;
           const int gi = q - n * gpr;
-          uint4 hi, lo;
-          split8(stg[j][0], stg[j][1], hi, lo);
-          uint4* d = reinterpret_cast<uint4*>(&lds[buf][n * stride + gi * 32]);
-          d[0] = hi;
-          d[1] = lo;
+          u32x4* d = reinterpret_cast<u32x4*>(&lds[buf][n * stride + gi * 32]);
+          d[0] = stg[j][0];
+          d[1] = stg[j][1];
         }
       }
     };
@@ -174,15 +223,46 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // Weight ring: slot i holds the fragments of the k-step congruent to i mod kRing.
-    uint4 ring0[kRing], ring1[kRing];
+    // Weight ring: slot i holds the fragments of the k-step congruent to i
+    // mod kRing.  Loads past the last k-step re-read the last one (always
+    // issued, never used), which keeps the loop free of branches.
+    u32x4 ring0[kRing], ring1[kRing];
 #pragma unroll
     for (int i = 0; i < kRing; ++i) {
-      if (i < nk) {
-        ring0[i] = *reinterpret_cast<const uint4*>(pa0 + i * kKStep);
-        ring1[i] = *reinterpret_cast<const uint4*>(pa1 + i * kKStep);
-      }
+      const int si = min(i, nk - 1);
+      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + si * kKStep);
+      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + si * kKStep);
     }
+
+    // One k-step: multiply ring slot I against the staged tokens of
+    // chunk-relative step s - ks, then refill the slot with step s + kRing.
+    // The refill is issued after the MFMAs that read the slot, into the same
+    // registers, and a scheduling barrier keeps it there, so each slot stays
+    // in place and kRing steps of loads are always in flight.
+    auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
+      constexpr int i = decltype(I)::value;
+      const unsigned char* bs = bb + (s - ks) * 128;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t < nt) {
+          // Column n of the product depends only on column n of B, so lanes
+          // past the bucket read its last token and their columns are
+          // simply not stored.
+          const int n = min(t * 16 + arow, c - 1);
+          const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * stride);
+          const u32x4 bh = bp[0];
+          const u32x4 bl = bp[1];
+          acc0[t] = mfma16x16x32(ring0[i], bh, acc0[t]);
+          acc0[t] = mfma16x16x32(ring0[i], bl, acc0[t]);
+          acc1[t] = mfma16x16x32(ring1[i], bh, acc1[t]);
+          acc1[t] = mfma16x16x32(ring1[i], bl, acc1[t]);
+        }
+      }
+      const int sn = min(s + kRing, nk - 1);
+      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + sn * kKStep);
+      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + sn * kKStep);
+      __builtin_amdgcn_sched_barrier(0);
+    };
 
     fetch(0, min(kcs, nk));
     for (int ks = 0, chunk = 0; ks < nk; ks += kcs, ++chunk) {
@@ -195,36 +275,16 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       if (ke < nk) fetch(ke, min(kcs, nk - ke));
 
       const unsigned char* bb = &lds[buf][kgrp * 32];
-      for (int sb = ks; sb < ke; sb += kRing) {  // ks is a multiple of kRing
-#pragma unroll
-        for (int i = 0; i < kRing; ++i) {
-          const int s = sb + i;
-          if (s < ke) {
-            const uint4 w0 = ring0[i];
-            const uint4 w1 = ring1[i];
-            if (s + kRing < nk) {
-              ring0[i] = *reinterpret_cast<const uint4*>(pa0 + (s + kRing) * kKStep);
-              ring1[i] = *reinterpret_cast<const uint4*>(pa1 + (s + kRing) * kKStep);
-            }
-            const unsigned char* bs = bb + (s - ks) * 128;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-              if (t < nt) {
-                // Column n of the product depends only on column n of B, so
-                // lanes past the bucket read its last token and their
-                // columns are simply not stored.
-                const int n = min(t * 16 + arow, c - 1);
-                const uint4* bp = reinterpret_cast<const uint4*>(bs + n * stride);
-                const uint4 bh = bp[0];
-                const uint4 bl = bp[1];
-                acc0[t] = mfma16x16x32(w0, bh, acc0[t]);
-                acc0[t] = mfma16x16x32(w0, bl, acc0[t]);
-                acc1[t] = mfma16x16x32(w1, bh, acc1[t]);
-                acc1[t] = mfma16x16x32(w1, bl, acc1[t]);
-              }
-            }
-          }
-        }
+      // ks is a multiple of kRing, so slot i always holds step sb + i.
+      const int kfull = ks + ((ke - ks) / kRing) * kRing;
+      for (int sb = ks; sb < kfull; sb += kRing) {
+        static_for<kRing>([&](auto I) { kstep(I, sb + decltype(I)::value, bb, ks); });
+      }
+      // Tail (only in the last chunk, when nk is not a multiple of kRing).
+      if (kfull < ke) {
+        static_for<kRing>([&](auto I) {
+          if (kfull + decltype(I)::value < ke) kstep(I, kfull + decltype(I)::value, bb, ks);
+        });
       }
     }
 
@@ -237,19 +297,24 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
         const size_t sl = (size_t)(s_begin + p0 + n);
         if (MODE == kUp) {
           if (ok0) {
-            float4 h;
-            h.x = silu(acc0[t][0]) * acc1[t][0];
-            h.y = silu(acc0[t][1]) * acc1[t][1];
-            h.z = silu(acc0[t][2]) * acc1[t][2];
-            h.w = silu(acc0[t][3]) * acc1[t][3];
-            *reinterpret_cast<float4*>(a.dst + sl * a.rows + r0 + rsub) = h;
+            // h for rows r0 + rsub .. + 3: half of one 8-value group of the
+            // split layout (high parts at +0, low parts at +16 bytes).
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) split_bf16(silu(acc0[t][i]) * acc1[t][i], hi[i], lo[i]);
+            const int col = r0 + rsub;
+            unsigned char* row = static_cast<unsigned char*>(a.dst) + sl * (size_t)a.rows * 4;
+            unsigned char* grp = row + (col / 8) * 32 + (col % 8) * 2;
+            *reinterpret_cast<uint2*>(grp) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+            *reinterpret_cast<uint2*>(grp + 16) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
           }
         } else {
+          float* y = static_cast<float*>(a.dst) + sl * a.rows;
           if (ok0)
-            *reinterpret_cast<float4*>(a.dst + sl * a.rows + r0 + rsub) =
+            *reinterpret_cast<float4*>(y + r0 + rsub) =
                 make_float4(acc0[t][0], acc0[t][1], acc0[t][2], acc0[t][3]);
           if (ok1)
-            *reinterpret_cast<float4*>(a.dst + sl * a.rows + r0 + 16 + rsub) =
+            *reinterpret_cast<float4*>(y + r0 + 16 + rsub) =
                 make_float4(acc1[t][0], acc1[t][1], acc1[t][2], acc1[t][3]);
         }
       }
@@ -268,6 +333,9 @@ static void launch_ffn(const FfnArgs& a, int E, hipStream_t s) {
 // bucket never exceeds T tokens), at most kMaxTiles.
 template <int MODE>
 static void launch_ffn_nt(const FfnArgs& a, int T, int E, hipStream_t s) {
+#ifdef ELDR_FFN_FORCE_NT
+  T = 16 * ELDR_FFN_FORCE_NT;
+#endif
   if (T <= 16)
     launch_ffn<MODE, 1>(a, E, s);
   else if (T <= 32)
@@ -278,9 +346,13 @@ static void launch_ffn_nt(const FfnArgs& a, int T, int E, hipStream_t s) {
 
 }  // namespace eldr
 
+// Workspace layout: h of every slot, then x, both as bf16 pairs (4 bytes a value).
+static size_t ws_h_bytes(const moe_dims& d) { return (size_t)d.T * d.K * d.I * 4; }
+static size_t ws_x_bytes(const moe_dims& d) { return (size_t)d.T * d.H * 4; }
+
 extern "C" size_t moe_ffn_workspace_bytes(moe_dims d) {
   if (eldr_host::check_dims(d) != MOE_OK) return 0;
-  return (size_t)d.T * d.K * d.I * sizeof(float);
+  return ws_h_bytes(d) + ws_x_bytes(d);
 }
 
 namespace {
@@ -299,7 +371,7 @@ int check_ffn_common(const moe_dims& d, const int32_t* offsets, const int32_t* p
 extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint16_t* w3,
                                  const int32_t* offsets, const int32_t* perm_token,
                                  const int32_t* union_ids, const int32_t* union_size, moe_dims d,
-                                 float* ws, size_t ws_bytes, void* stream) {
+                                 void* ws, size_t ws_bytes, void* stream) {
   using namespace eldr_host;
   int st = check_dims(d);
   if (st != MOE_OK) return st;
@@ -309,13 +381,21 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint1
   if (st != MOE_OK) return st;
   if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
-  eldr::FfnArgs up{x, w1, w3, offsets, perm_token, union_ids, union_size, ws, d.I, d.H, 0};
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* wsb = reinterpret_cast<unsigned char*>(ws);
+  uint4* xs = reinterpret_cast<uint4*>(wsb + ws_h_bytes(d));
+  const int ngroups = d.T * (d.H / 8);
+  hipLaunchKernelGGL(eldr::split_rows_kernel, dim3((ngroups + 255) / 256), dim3(256), 0, s, x,
+                     ngroups, xs);
+  st = launch_status();
+  if (st != MOE_OK) return st;
+  eldr::FfnArgs up{xs, w1, w3, offsets, perm_token, union_ids, union_size, ws, d.I, d.H, 0};
   up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
-  eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.E, s);
   return launch_status();
 }
 
-extern "C" int moe_expert_ffn_down(const float* ws, const uint16_t* w2, const int32_t* offsets,
+extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offsets,
                                    const int32_t* perm_token, const int32_t* union_ids,
                                    const int32_t* union_size, moe_dims d, size_t ws_bytes,
                                    float* y_perm, void* stream) {
@@ -328,8 +408,8 @@ extern "C" int moe_expert_ffn_down(const float* ws, const uint16_t* w2, const in
   if (st != MOE_OK) return st;
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
-  eldr::FfnArgs down{ws, w2, nullptr, offsets, perm_token, union_ids, union_size, y_perm, d.H, d.I,
-                     0};
+  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, nullptr, offsets, perm_token,
+                     union_ids, union_size, y_perm, d.H, d.I, 0};
   down.tiles =
       (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
   eldr::launch_ffn_nt<eldr::kDown>(down, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
