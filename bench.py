@@ -10,10 +10,12 @@ To keep the 256 MB Infinity Cache from serving repeated weight reads, step i
 uses weight copy i mod R, with R copies whose union bytes together exceed
 2 GB (all copies hold the same bits).
 
-Printed: one JSON line with the layer's achieved algorithmic GB/s (the
-metric), the roofline of the dominant kernel (the FFN up projection, timed
-with HIP events on the stream it runs on), and the CPU oracle's rate on the
-host cores.  ``--sweep PATH`` also writes the controlled-union and batch
+The timed layer steps are HIP graph replays (one graph per weight copy,
+captured from the same calls), so host launch cost is not in the GPU
+timeline.  Printed: one JSON line with the layer's achieved algorithmic GB/s
+(the metric), the roofline of the dominant kernel (the FFN up projection,
+timed with HIP events on the stream it runs on), and the CPU oracle's rate on
+the host cores.  ``--sweep PATH`` also writes the controlled-union and batch
 sweeps (one JSON object per point) to PATH.
 """
 from __future__ import annotations
@@ -102,21 +104,42 @@ class Bench:
         torch.cuda.synchronize()
         return int(self.buf.union_size.item())
 
+    def capture(self, routing=None) -> list:
+        """One HIP graph per weight copy, each holding one whole layer step."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for i in range(len(self.weights)):
+                self.step(i, routing)
+        torch.cuda.current_stream().wait_stream(side)
+        graphs = []
+        for i in range(len(self.weights)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.step(i, routing)
+            graphs.append(g)
+        torch.cuda.synchronize()
+        return graphs
+
     def time(self, steps: int, warmup: int, routing=None) -> dict:
+        # Whole layer: graph replays, so host launch cost stays out of the GPU timeline.
+        graphs = self.capture(routing)
         for i in range(warmup):
-            self.step(i, routing)
+            graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(self.stream)
         for i in range(steps):
-            self.step(i, routing)
+            graphs[i % len(graphs)].replay()
         t1.record(self.stream)
         torch.cuda.synchronize()
         layer_ms = t0.elapsed_time(t1) / steps
+        del graphs
         # Per-kernel durations of the FFN halves, with events around each
-        # launch on the stream it runs on (a separate pass, so the events do
-        # not perturb the whole-layer timing above).
+        # launch on the stream it runs on (a separate eager pass, so the
+        # events do not perturb the whole-layer timing above; the host runs
+        # ahead of the GPU here, so the kernels still run back to back).
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
         for i in range(steps):
             self.step(i, routing, evs[i])

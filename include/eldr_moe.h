@@ -116,8 +116,8 @@ int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* of
                int32_t* union_size, void* stream);
 
 /* Bytes of device workspace moe_expert_ffn needs for dims d: the SwiGLU
- * activations of every slot and a copy of x, each stored as pairs of bf16
- * values (4 bytes a value): 4 * (T*K*I + T*H).  0 when T == 0. */
+ * activations of every slot, stored as pairs of bf16 values (4 bytes a
+ * value): 4 * T*K*I.  0 when T == 0. */
 size_t moe_ffn_workspace_bytes(moe_dims d);
 
 /*

@@ -7,25 +7,38 @@ namespace eldr {
 
 constexpr int kCombineThreads = 256;
 
+// One workgroup row per token: the token's K slots and weights are the same
+// for every thread (scalar loads), and all K expert rows are requested before
+// the first one is used.
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
     const float* __restrict__ y, const int32_t* __restrict__ pair_pos,
     const float* __restrict__ w, int T, int H, int K, float* __restrict__ out) {
   const int t = blockIdx.y;
   const int h4 = blockIdx.x * kCombineThreads + threadIdx.x;
-  if (h4 * 4 >= H) return;
   const int P = T * K;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < K; ++j) {
-    const int p = pair_pos[t * K + j];
-    if (p < 0 || p >= P) continue;
-    const float wj = w[t * K + j];
-    const float4 v = reinterpret_cast<const float4*>(y + (size_t)p * H)[h4];
-    acc.x = fmaf(wj, v.x, acc.x);
-    acc.y = fmaf(wj, v.y, acc.y);
-    acc.z = fmaf(wj, v.z, acc.z);
-    acc.w = fmaf(wj, v.w, acc.w);
+  const bool live = h4 * 4 < H;
+  float4 v[MOE_MAX_K];
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_K; ++j) {
+    if (j < K) {
+      const int p = pair_pos[t * K + j];
+      const bool ok = live && p >= 0 && p < P;
+      v[j] = ok ? reinterpret_cast<const float4*>(y + (size_t)p * H)[h4]
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   }
-  reinterpret_cast<float4*>(out + (size_t)t * H)[h4] = acc;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < MOE_MAX_K; ++j) {
+    if (j < K) {
+      const float wj = w[t * K + j];
+      acc.x = fmaf(wj, v[j].x, acc.x);
+      acc.y = fmaf(wj, v[j].y, acc.y);
+      acc.z = fmaf(wj, v[j].z, acc.z);
+      acc.w = fmaf(wj, v[j].w, acc.w);
+    }
+  }
+  if (live) reinterpret_cast<float4*>(out + (size_t)t * H)[h4] = acc;
 }
 
 }  // namespace eldr

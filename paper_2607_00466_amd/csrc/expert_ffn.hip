@@ -56,8 +56,7 @@ __host__ __device__ constexpr int lds_buf_bytes() {
 enum FfnMode { kUp = 0, kDown = 1 };
 
 struct FfnArgs {
-  const uint4* src;            // activations as bf16 pairs (see split_rows_kernel):
-                               // up: x [T, H]; down: h [T*K, I]
+  const uint4* src;            // up: x [T, H] fp32; down: h [T*K, I] as bf16 pairs
   const uint16_t* wa;          // up: W1 [E, I, H]; down: W2 [E, H, I]
   const uint16_t* wb;          // up: W3 [E, I, H]; down: unused
   const int32_t* offsets;      // [E+1]
@@ -97,32 +96,36 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Pack 8 fp32 values as 8 bf16 high parts and 8 bf16 low parts.
-__device__ __forceinline__ void split8(const float4& a, const float4& b, uint4& hi, uint4& lo) {
-  const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  uint32_t h[8], l[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) split_bf16(v[i], h[i], l[i]);
-  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
-  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Split two fp32 values into bf16 high parts and rounded remainders with the
+// packed round-to-nearest-even convert: hi = rne(v), lo = rne(v - hi).
+__device__ __forceinline__ void split2(uint32_t a, uint32_t b, uint32_t& hi, uint32_t& lo) {
+  const f32x2 v = {__uint_as_float(a), __uint_as_float(b)};
+  const bf16x2 h = __builtin_convertvector(v, bf16x2);
+  const f32x2 r = v - __builtin_convertvector(h, f32x2);
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
+}
+
+// 8 fp32 values (as raw bits) -> 8 bf16 high parts and 8 bf16 low parts.
+__device__ __forceinline__ void split8_pk(const u32x4& a, const u32x4& b, u32x4& hi, u32x4& lo) {
+  uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
+  split2(a.x, a.y, h0, l0);
+  split2(a.z, a.w, h1, l1);
+  split2(b.x, b.y, h2, l2);
+  split2(b.z, b.w, h3, l3);
+  hi = u32x4{h0, h1, h2, h3};
+  lo = u32x4{l0, l1, l2, l3};
 }
 
 // Activations enter the MFMA B operand as a pair of bf16 numbers (high
-// part, rounded remainder).  In memory a row of K values is K / 8 groups of
-// 32 bytes: 8 bf16 high parts, then the 8 matching low parts -- the same
-// 4 bytes per value as fp32, and exactly the layout staged in LDS, so that
-// staging is a plain copy.  This kernel writes x in that form, one group per
-// thread.
-__global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict__ src, int ngroups,
-                                                         uint4* __restrict__ dst) {
-  const int g = blockIdx.x * 256 + threadIdx.x;
-  if (g >= ngroups) return;
-  const float4* p = reinterpret_cast<const float4*>(src) + 2 * (size_t)g;
-  uint4 hi, lo;
-  split8(p[0], p[1], hi, lo);
-  dst[2 * (size_t)g] = hi;
-  dst[2 * (size_t)g + 1] = lo;
-}
+// part, rounded remainder).  In LDS, and for h in the workspace, a row of K
+// values is K / 8 groups of 32 bytes: 8 bf16 high parts, then the 8 matching
+// low parts -- the same 4 bytes per value as fp32.  The up kernel stages x
+// from fp32 and splits it on the way into LDS; its epilogue writes h already
+// split, so the down kernel stages h with a plain copy.
 
 template <int MODE, int NT>
 __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
@@ -139,10 +142,15 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
 
   // ---- which (expert, row band) this workgroup owns -----------------------
   const int bid = blockIdx.x;
+#ifdef ELDR_MAP_PLAIN
+  const int u = bid / a.tiles;
+  const int tile = bid - u * a.tiles;
+#else
   const int xcd = bid % kNumXcd;
   const int slot = bid / kNumXcd;
   const int u = (slot / a.tiles) * kNumXcd + xcd;
   const int tile = slot % a.tiles;
+#endif
   const int U = *a.union_size;
   if (u >= U) return;  // also covers U < 0 (invalid routing)
   const int e = a.union_ids[u];
@@ -167,6 +175,25 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   const uint16_t* pa0 = a.wa + (size_t)e * expert_w + (size_t)(ra0 + arow) * K + kgrp * 8;
   const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) + (size_t)e * expert_w +
                         (size_t)(ra1 + arow) * K + kgrp * 8;
+
+  // Weight ring: slot i holds the fragments of the k-step congruent to i
+  // mod kRing.  Loads past the last k-step re-read the last one (always
+  // issued, never used), which keeps the loop free of branches.
+  u32x4 ring0[kRing], ring1[kRing];
+  auto ring_prologue = [&]() {
+#pragma unroll
+    for (int i = 0; i < kRing; ++i) {
+      const int si = min(i, nk - 1);
+      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + si * kKStep);
+      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + si * kKStep);
+#ifdef ELDR_RING_ORDERED
+      __builtin_amdgcn_sched_barrier(0);
+#endif
+    }
+  };
+#ifdef ELDR_EARLY_RING
+  ring_prologue();
+#endif
 
   for (int p0 = 0; p0 < c_total; p0 += NT * 16) {
     const int c = min(NT * 16, c_total - p0);
@@ -210,8 +237,15 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
           const int n = q / gpr;
           const int gi = q - n * gpr;
           u32x4* d = reinterpret_cast<u32x4*>(&lds[buf][n * stride + gi * 32]);
-          d[0] = stg[j][0];
-          d[1] = stg[j][1];
+          if (MODE == kUp) {
+            u32x4 hi, lo;
+            split8_pk(stg[j][0], stg[j][1], hi, lo);
+            d[0] = hi;
+            d[1] = lo;
+          } else {
+            d[0] = stg[j][0];
+            d[1] = stg[j][1];
+          }
         }
       }
     };
@@ -223,16 +257,11 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // Weight ring: slot i holds the fragments of the k-step congruent to i
-    // mod kRing.  Loads past the last k-step re-read the last one (always
-    // issued, never used), which keeps the loop free of branches.
-    u32x4 ring0[kRing], ring1[kRing];
-#pragma unroll
-    for (int i = 0; i < kRing; ++i) {
-      const int si = min(i, nk - 1);
-      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + si * kKStep);
-      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + si * kKStep);
-    }
+#ifdef ELDR_EARLY_RING
+    if (p0 > 0) ring_prologue();
+#else
+    ring_prologue();
+#endif
 
     // One k-step: multiply ring slot I against the staged tokens of
     // chunk-relative step s - ks, then refill the slot with step s + kRing.
@@ -324,8 +353,12 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
 
 template <int MODE, int NT>
 static void launch_ffn(const FfnArgs& a, int E, hipStream_t s) {
+#ifdef ELDR_MAP_PLAIN
+  const dim3 grid(E * a.tiles);
+#else
   const int groups = (E + kNumXcd - 1) / kNumXcd;
   const dim3 grid(kNumXcd * a.tiles * groups);
+#endif
   hipLaunchKernelGGL((ffn_kernel<MODE, NT>), grid, dim3(kFfnThreads), 0, s, a);
 }
 
@@ -346,13 +379,10 @@ static void launch_ffn_nt(const FfnArgs& a, int T, int E, hipStream_t s) {
 
 }  // namespace eldr
 
-// Workspace layout: h of every slot, then x, both as bf16 pairs (4 bytes a value).
-static size_t ws_h_bytes(const moe_dims& d) { return (size_t)d.T * d.K * d.I * 4; }
-static size_t ws_x_bytes(const moe_dims& d) { return (size_t)d.T * d.H * 4; }
-
+// Workspace: h of every slot as bf16 pairs (4 bytes a value).
 extern "C" size_t moe_ffn_workspace_bytes(moe_dims d) {
   if (eldr_host::check_dims(d) != MOE_OK) return 0;
-  return ws_h_bytes(d) + ws_x_bytes(d);
+  return (size_t)d.T * d.K * d.I * 4;
 }
 
 namespace {
@@ -382,14 +412,8 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint1
   if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  unsigned char* wsb = reinterpret_cast<unsigned char*>(ws);
-  uint4* xs = reinterpret_cast<uint4*>(wsb + ws_h_bytes(d));
-  const int ngroups = d.T * (d.H / 8);
-  hipLaunchKernelGGL(eldr::split_rows_kernel, dim3((ngroups + 255) / 256), dim3(256), 0, s, x,
-                     ngroups, xs);
-  st = launch_status();
-  if (st != MOE_OK) return st;
-  eldr::FfnArgs up{xs, w1, w3, offsets, perm_token, union_ids, union_size, ws, d.I, d.H, 0};
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w1, w3, offsets, perm_token, union_ids,
+                   union_size, ws, d.I, d.H, 0};
   up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
   eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.E, s);
   return launch_status();

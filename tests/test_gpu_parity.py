@@ -225,3 +225,44 @@ def test_gpt_oss_layer_sampled():
     sub = O.moe_layer_routed(layer.x_np[sample], ids[sample], g["weights"][sample].astype(np.float64),
                              w1, w3, w2, GPTOSS.E)
     G.check_output(g["out"][sample], sub["out"], "sampled tokens")
+
+
+def test_graph_replay_matches_eager():
+    # The layer captured as a HIP graph (as the benchmark times it) gives the
+    # eager result on every replay, with eager work and syncs in between, and
+    # follows new input values written in place.
+    G.say("case: qwen layer T=64 gate-routed, HIP graph replays vs eager")
+    layer = G.Layer(QWEN, 64, experts_on_host=False)
+    d, buf = layer.d, layer.buf
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.w1, layer.w3, layer.w2, d, buf)  # noqa: E731
+    run()
+    torch.cuda.synchronize()
+    eager = buf.out.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        buf.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf.out, eager), f"replay {rep}"
+        scratch = torch.randn(1024, device="cuda") * 2  # unrelated eager work between replays
+        torch.cuda.synchronize()
+        del scratch
+    x2 = torch.from_numpy(synth.hidden_states(64, QWEN.H, seed=5)).cuda()
+    layer.x.copy_(x2)
+    run()
+    torch.cuda.synchronize()
+    eager2 = buf.out.clone()
+    buf.out.zero_()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(buf.out, eager2)
+    assert not torch.equal(eager, eager2)
