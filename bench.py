@@ -39,6 +39,28 @@ from paper_2607_00466_amd import synth  # noqa: E402
 METRIC = "MoE decode-layer µs and achieved HBM GB/s vs distinct-expert union (Qwen3-30B-A3B shape)"
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 2 << 30
+PROFILE = os.path.join(ROOT, "profiles", "moe_layer_qwen3_30b_a3b_T64.md")
+FFN_SOURCE = os.path.join(ROOT, "paper_2607_00466_amd", "csrc", "expert_ffn.hip")
+
+
+def measured_traffic() -> int | None:
+    """HBM bytes per FFN-up launch from the committed rocprofv3 counter profile
+    (FETCH_SIZE + WRITE_SIZE, calibrated against a 1 GiB copy), or None when the
+    kernel source has changed since the counters were taken."""
+    import hashlib
+
+    try:
+        text = open(PROFILE).read()
+    except OSError:
+        return None
+    fields = dict(l.split(": ", 1) for l in text.splitlines() if ": " in l and not l.startswith(("|", "#", "`")))
+    src = hashlib.sha256(open(FFN_SOURCE, "rb").read()).hexdigest()[:16]
+    if fields.get("expert_ffn_source_sha256_16", "").strip() != src:
+        return None
+    try:
+        return int(float(fields["traffic_bytes_per_launch (ffn up, read + write)"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def log(msg: str) -> None:
@@ -261,7 +283,7 @@ def main() -> int:
         "ffn_down_us": round(r["down_ms"] * 1e3, 2),
         "roofline": {"bound": "hbm", "kernel": "ffn_kernel<up> (moe_expert_ffn_up)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "bytes_per_launch": ub},
     }
     if args.cpu_seconds > 0:

@@ -6,15 +6,18 @@
 // bound by HBM bandwidth.  The design follows from that:
 //
 // * Two launches.  "up" computes h = silu(W1 x) * (W3 x) for every slot into
-//   a small fp32 workspace; "down" computes y = W2 h.  Within each launch a
-//   workgroup owns one expert and a band of output rows, and streams that
-//   band's bf16 weights from HBM exactly once (128-bit loads straight into
-//   the MFMA A operand), for all of the expert's tokens at once.
-// * The expert's tokens (at most 128 per pass) are gathered, split into a
-//   pair of bf16 values (high part + rounded remainder) and staged in LDS in
+//   the workspace (as bf16 pairs, see below); "down" computes y = W2 h.
+//   Within each launch a workgroup owns one expert and a band of output rows
+//   and streams that band's bf16 weights from HBM exactly once (128-bit loads
+//   straight into the MFMA A operand), for all of the expert's tokens at once.
+// * The expert's tokens (at most 64 per pass) are gathered, carried as a pair
+//   of bf16 values (high part + rounded remainder) and staged in LDS in
 //   k-chunks, double-buffered, shared by the workgroup's four waves; each
 //   wave reads them as the MFMA B operand.  Tokens are padded to a multiple
-//   of 16 only in registers (lanes beyond the bucket feed zeros).
+//   of 16 only in registers (lanes past the bucket repeat its last token and
+//   their output columns are not stored).
+// * Each wave keeps a ring of weight fragments for the next k-steps in
+//   flight; a refill is issued right after the MFMAs that consumed its slot.
 // * The grid is sized for E experts; a workgroup reads the union size on the
 //   device and returns at once if its slot is past it, so inactive experts
 //   cost one scalar load and no host synchronisation is needed.
@@ -142,15 +145,10 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
 
   // ---- which (expert, row band) this workgroup owns -----------------------
   const int bid = blockIdx.x;
-#ifdef ELDR_MAP_PLAIN
-  const int u = bid / a.tiles;
-  const int tile = bid - u * a.tiles;
-#else
   const int xcd = bid % kNumXcd;
   const int slot = bid / kNumXcd;
   const int u = (slot / a.tiles) * kNumXcd + xcd;
   const int tile = slot % a.tiles;
-#endif
   const int U = *a.union_size;
   if (u >= U) return;  // also covers U < 0 (invalid routing)
   const int e = a.union_ids[u];
@@ -186,14 +184,8 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       const int si = min(i, nk - 1);
       ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + si * kKStep);
       ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + si * kKStep);
-#ifdef ELDR_RING_ORDERED
-      __builtin_amdgcn_sched_barrier(0);
-#endif
     }
   };
-#ifdef ELDR_EARLY_RING
-  ring_prologue();
-#endif
 
   for (int p0 = 0; p0 < c_total; p0 += NT * 16) {
     const int c = min(NT * 16, c_total - p0);
@@ -257,11 +249,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-#ifdef ELDR_EARLY_RING
-    if (p0 > 0) ring_prologue();
-#else
     ring_prologue();
-#endif
 
     // One k-step: multiply ring slot I against the staged tokens of
     // chunk-relative step s - ks, then refill the slot with step s + kRing.
@@ -353,12 +341,8 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
 
 template <int MODE, int NT>
 static void launch_ffn(const FfnArgs& a, int E, hipStream_t s) {
-#ifdef ELDR_MAP_PLAIN
-  const dim3 grid(E * a.tiles);
-#else
   const int groups = (E + kNumXcd - 1) / kNumXcd;
   const dim3 grid(kNumXcd * a.tiles * groups);
-#endif
   hipLaunchKernelGGL((ffn_kernel<MODE, NT>), grid, dim3(kFfnThreads), 0, s, a);
 }
 
