@@ -90,7 +90,9 @@ class Bench:
         self.wg_np = synth.gate_weights(shape, seed)
         self.x = torch.from_numpy(self.x_np).cuda()
         self.wg = torch.from_numpy(self.wg_np).cuda()
-        self.weights = [synth.expert_weights(shape, seed, device="cuda")]
+        raw = synth.expert_weights(shape, seed, device="cuda")
+        self.raw_weights = raw  # row-major, for the CPU baseline
+        self.weights = [B.pack_expert_weights(*raw)]  # packed once, before any timing
         self.buf = B.LayerBuffers.allocate(self.d)
         self.stream = torch.cuda.current_stream()
 
@@ -178,7 +180,7 @@ def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:
 
     from oracle import moe_oracle
 
-    w1, w3, w2 = (synth.bf16_bits(w) for w in bench.weights[0])
+    w1, w3, w2 = (synth.bf16_bits(w) for w in bench.raw_weights)
     runs, t_total = 0, 0.0
     with threadpool_limits(limits=1):
         while t_total < budget_s and runs < 50:

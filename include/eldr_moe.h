@@ -28,10 +28,12 @@
  *   throws or exits across this boundary.
  * - Layouts are row-major.  Float data is IEEE binary32 ("fp32").  bf16 data
  *   is passed as raw 16-bit patterns (uint16_t), the upper half of a binary32.
- * - Expert weights are stored [out, in] so that each output neuron's weights
- *   are contiguous along the reduction axis:
+ * - Weights are defined row-major [out, in] (each output neuron's weights
+ *   contiguous along the reduction axis):
  *     w_gate [E, H] fp32; w1, w3 [E, I, H] bf16; w2 [E, H, I] bf16.
  *   The math is y = W2 (silu(W1 x) * (W3 x)) with silu(z) = z / (1 + e^-z).
+ *   The expert FFN takes w1, w3 and w2 *packed* by moe_pack_weights (a
+ *   permutation done once, when the model is loaded; see below).
  * - Pointers to fp32 or bf16 arrays must be 16-byte aligned (the kernels use
  *   128-bit loads and stores); int32 arrays 4-byte aligned.
  * - T = 0 (an empty batch) is accepted everywhere: nothing is computed except
@@ -115,6 +117,22 @@ int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* of
                int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,
                int32_t* union_size, void* stream);
 
+/*
+ * moe_pack_weights -- permute one expert weight tensor [E, R, K] (bf16,
+ * row-major [out, in]) into the fragment layout the expert FFN streams.
+ * Output element order: for each expert e, 16-row band b (R / 16 of them),
+ * k-step s (K / 32 of them) and lane l (0..63), the 8 values
+ *   src[e, 16 b + (l % 16), 32 s + 8 (l / 16) + j], j = 0..7,
+ * i.e. one 16 x 32 MFMA A fragment per 1 KB, lanes in order, so that each
+ * load of the FFN reads 1 KB of consecutive memory.  Values and size are
+ * unchanged (E * R * K bf16).  Call once per tensor, off the decode path:
+ * w1 and w3 with (R, K) = (I, H), w2 with (R, K) = (H, I).
+ * src and dst are distinct 16-byte-aligned device buffers; R % 16 == 0 and
+ * K % 32 == 0.  Asynchronous on `stream`.
+ */
+int moe_pack_weights(const uint16_t* src, int32_t E, int32_t R, int32_t K, uint16_t* dst,
+                     void* stream);
+
 /* Bytes of device workspace moe_expert_ffn needs for dims d: the SwiGLU
  * activations of every slot, stored as pairs of bf16 values (4 bytes a
  * value): 4 * T*K*I.  0 when T == 0. */
@@ -135,7 +153,8 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * The grid is sized for E experts and reads union_size on the device, so no
  * host synchronisation is needed between moe_bucket and this call.
  *
- * x [T, H] fp32; w1, w3 [E, I, H] bf16; w2 [E, H, I] bf16; offsets [E+1],
+ * x [T, H] fp32; w1, w3 ([E, I, H]) and w2 ([E, H, I]) bf16 packed by
+ * moe_pack_weights; offsets [E+1],
  * perm_token [T*K], union_ids [E], union_size [1] int32 (moe_bucket output).
  * y_perm [T*K, H] fp32 output (rows of slots whose expert is not in the
  * union are not written).  ws: device workspace of at least

@@ -54,6 +54,8 @@ _SIGNATURES = {
     "moe_expert_ffn_down": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, MoeDims, ctypes.c_size_t,
                                            _vp, _vp]),
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
+    "moe_pack_weights": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
+                                        _vp]),
 }
 
 _lib = None
@@ -193,6 +195,24 @@ def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: M
         ws_bytes, _ptr(y_perm), _stream(stream)))
 
 
+def moe_pack_weights(src, dst=None, stream=None) -> torch.Tensor:
+    """Pack one expert weight tensor [E, R, K] (bf16) for the expert FFN; returns dst."""
+    if src.dim() != 3:
+        raise ValueError("src: expected [E, R, K]")
+    E, R, K = (int(v) for v in src.shape)
+    _need(src, "src", torch.bfloat16, E * R * K)
+    if dst is None:
+        dst = torch.empty_like(src)
+    _need(dst, "dst", torch.bfloat16, E * R * K)
+    _check("moe_pack_weights", load().moe_pack_weights(_ptr(src), E, R, K, _ptr(dst), _stream(stream)))
+    return dst
+
+
+def pack_expert_weights(w1, w3, w2, stream=None):
+    """Pack (w1 [E,I,H], w3 [E,I,H], w2 [E,H,I]) for moe_expert_ffn."""
+    return tuple(moe_pack_weights(w, stream=stream) for w in (w1, w3, w2))
+
+
 def moe_combine(y_perm, pair_pos, topk_w, d: MoeDims, out, stream=None) -> None:
     _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
     _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
@@ -244,6 +264,8 @@ class LayerBuffers:
 
 def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
     """One decode-step MoE layer: the four calls back to back on one stream.
+
+    w1, w3 and w2 are the expert weights packed by ``pack_expert_weights``.
 
     ``routing=(topk_ids, topk_w)`` bypasses the gate (the ids are copied into
     ``buf``).  Returns ``buf.out``.

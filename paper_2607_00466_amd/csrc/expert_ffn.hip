@@ -10,6 +10,8 @@
 //   Within each launch a workgroup owns one expert and a band of output rows
 //   and streams that band's bf16 weights from HBM exactly once (128-bit loads
 //   straight into the MFMA A operand), for all of the expert's tokens at once.
+//   Weights come packed by moe_pack_weights, so each load instruction reads
+//   one contiguous 1 KB MFMA fragment.
 // * The expert's tokens (at most 64 per pass) are gathered, carried as a pair
 //   of bf16 values (high part + rounded remainder) and staged in LDS in
 //   k-chunks, double-buffered, shared by the workgroup's four waves; each
@@ -38,6 +40,7 @@ namespace eldr {
 constexpr int kFfnThreads = 256;  // 4 waves
 constexpr int kFfnWaves = kFfnThreads / kWave;
 constexpr int kKStep = 32;        // k per MFMA
+constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
 constexpr int kMaxTiles = 4;      // token tiles of 16 per pass: at most 64 tokens per pass
 
 // k-steps of weights in flight per wave (the prefetch depth of the ring).
@@ -166,13 +169,17 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE>();
   const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE>());
 
-  // A operand: lane reads row (lane % 16) of its tile, k-group (lane / 16).
-  const size_t expert_w = (size_t)a.rows * K;
+  // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
+  // (lane / 16).  Weights are packed (moe_pack_weights): the 64 lane pieces of
+  // one tile and k-step are a contiguous 1 KB fragment, and a tile's k-steps
+  // follow each other, so step s of a tile is at tile_base + s * 512 values.
   const int arow = lane & 15;
   const int kgrp = lane >> 4;
-  const uint16_t* pa0 = a.wa + (size_t)e * expert_w + (size_t)(ra0 + arow) * K + kgrp * 8;
-  const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) + (size_t)e * expert_w +
-                        (size_t)(ra1 + arow) * K + kgrp * 8;
+  const size_t tiles_per_expert = (size_t)(a.rows / 16);
+  const uint16_t* pa0 =
+      a.wa + ((e * tiles_per_expert + ra0 / 16) * nk) * kFragElems + lane * 8;
+  const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) +
+                        ((e * tiles_per_expert + ra1 / 16) * nk) * kFragElems + lane * 8;
 
   // Weight ring: slot i holds the fragments of the k-step congruent to i
   // mod kRing.  Loads past the last k-step re-read the last one (always
@@ -182,8 +189,8 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
 #pragma unroll
     for (int i = 0; i < kRing; ++i) {
       const int si = min(i, nk - 1);
-      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + si * kKStep);
-      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + si * kKStep);
+      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)si * kFragElems);
+      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)si * kFragElems);
     }
   };
 
@@ -276,8 +283,8 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
         }
       }
       const int sn = min(s + kRing, nk - 1);
-      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + sn * kKStep);
-      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + sn * kKStep);
+      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)sn * kFragElems);
+      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)sn * kFragElems);
       __builtin_amdgcn_sched_barrier(0);
     };
 

@@ -17,7 +17,8 @@ def lib():
 
 def test_exports_every_declared_function(lib):
     names = B.header_functions()
-    assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_combine",
+    assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_expert_ffn_up",
+            "moe_expert_ffn_down", "moe_combine", "moe_pack_weights",
             "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
@@ -106,3 +107,14 @@ def test_binding_requires_device_tensors():
     with pytest.raises(ValueError):
         B.moe_combine(torch.zeros(4, 64), torch.zeros(4, dtype=torch.int32), torch.zeros(2, 2), d,
                       torch.zeros(2, 64))
+
+
+def test_pack_arguments_rejected(lib):
+    FAKE2 = ctypes.c_void_p(0x20000)
+    assert lib.moe_pack_weights(FAKE, -1, 16, 32, FAKE2, None) == B.MOE_ERR_INVALID
+    assert lib.moe_pack_weights(FAKE, 2, 24, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED   # R % 16
+    assert lib.moe_pack_weights(FAKE, 2, 16, 48, FAKE2, None) == B.MOE_ERR_UNSUPPORTED   # K % 32
+    assert lib.moe_pack_weights(None, 2, 16, 32, FAKE2, None) == B.MOE_ERR_INVALID
+    assert lib.moe_pack_weights(FAKE, 2, 16, 32, FAKE, None) == B.MOE_ERR_INVALID       # in place
+    assert lib.moe_pack_weights(FAKE_MIS, 2, 16, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED
+    assert lib.moe_pack_weights(None, 0, 16, 32, None, None) == B.MOE_OK                # empty

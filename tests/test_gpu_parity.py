@@ -149,7 +149,7 @@ def test_empty_batch():
     buf.union_size.fill_(77)
     buf.counts.fill_(5)
     x = torch.empty((0, TINY.H), device="cuda")
-    w1, w3, w2 = synth.expert_weights(TINY, device="cuda")
+    w1, w3, w2 = B.pack_expert_weights(*synth.expert_weights(TINY, device="cuda"))
     B.moe_layer(x, torch.zeros((TINY.E, TINY.H), device="cuda"), w1, w3, w2, d, buf)
     torch.cuda.synchronize()
     assert int(buf.union_size.item()) == 0
@@ -234,7 +234,7 @@ def test_graph_replay_matches_eager():
     G.say("case: qwen layer T=64 gate-routed, HIP graph replays vs eager")
     layer = G.Layer(QWEN, 64, experts_on_host=False)
     d, buf = layer.d, layer.buf
-    run = lambda: B.moe_layer(layer.x, layer.wg, layer.w1, layer.w3, layer.w2, d, buf)  # noqa: E731
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p1, layer.p3, layer.p2, d, buf)  # noqa: E731
     run()
     torch.cuda.synchronize()
     eager = buf.out.clone()
@@ -266,3 +266,16 @@ def test_graph_replay_matches_eager():
     torch.cuda.synchronize()
     assert torch.equal(buf.out, eager2)
     assert not torch.equal(eager, eager2)
+
+
+@pytest.mark.parametrize("E,R,K", [(3, 16, 32), (2, 48, 96), (128, 768, 2048), (5, 2880, 2880)])
+def test_pack_weights_is_the_documented_permutation(E, R, K):
+    G.say(f"case: pack E={E} R={R} K={K}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(E * 1000 + R)
+    w = torch.randn((E, R, K), generator=g, device="cuda").to(torch.bfloat16)
+    packed = synth.bf16_bits(B.moe_pack_weights(w))
+    src = synth.bf16_bits(w)
+    # fragment (e, band, step) holds, lane by lane, src[e, 16 band + l % 16, 32 step + 8 (l // 16) + j]
+    ref = src.reshape(E, R // 16, 16, K // 32, 4, 8).transpose(0, 1, 3, 4, 2, 5).reshape(-1)
+    assert np.array_equal(packed.reshape(-1), ref)
