@@ -234,6 +234,134 @@ def sweep(path: str, steps: int, warmup: int) -> None:
     log(f"fit: t = {a:.2f} + {b:.3f} U us (R^2 {r2:.4f})")
 
 
+class MultiLayer:
+    """A decode step over many distinct MoE layers (packed weights resident in HBM).
+
+    ``n_resident`` distinct layers are allocated; a step of ``n_layers`` layers
+    cycles through them (each layer's weights far exceed the Infinity Cache,
+    so a cycled layer is still read from HBM).
+    """
+
+    def __init__(self, shape: synth.LayerShape, T: int, n_layers: int, n_resident: int, seed: int = 0):
+        self.shape, self.T, self.n_layers = shape, T, n_layers
+        self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        self.layers = []
+        for layer in range(n_resident):
+            raw = synth.expert_weights(shape, seed, layer, device="cuda")
+            packed = B.pack_expert_weights(*raw)
+            del raw
+            x = torch.from_numpy(synth.hidden_states(T, shape.H, seed, layer)).cuda()
+            wg = torch.from_numpy(synth.gate_weights(shape, seed, layer)).cuda()
+            self.layers.append((x, wg, packed))
+        torch.cuda.synchronize()
+        self.bufs = [B.LayerBuffers.allocate(self.d) for _ in range(n_layers)]
+
+    def step(self, routing=None) -> None:
+        """One decode step; routing[l] = (ids, w) device tensors, or None for the gate."""
+        for l in range(self.n_layers):
+            x, wg, (w1, w3, w2) = self.layers[l % len(self.layers)]
+            r = None if routing is None else routing[l]
+            B.moe_layer(x, wg, w1, w3, w2, self.d, self.bufs[l], routing=r)
+
+    def unions(self) -> list[int]:
+        torch.cuda.synchronize()
+        return [int(b.union_size.item()) for b in self.bufs]
+
+    def time(self, steps: int, warmup: int, routing=None) -> float:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.step(routing)
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step(routing)
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(steps):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        del g
+        return t0.elapsed_time(t1) / steps
+
+
+def domain_workload(path: str, steps: int, warmup: int) -> None:
+    """48 Qwen3-30B-A3B-shaped layers per step, T=128, domain-clustered routing:
+    a same-domain batch per domain vs a batch mixed evenly over the 8 domains."""
+    shape = synth.SHAPES["qwen3_30b_a3b"]
+    model = synth.DomainModel()
+    L, T = 48, 128
+    ml = MultiLayer(shape, T, L, L)
+    subsets = synth.domain_subsets(model, L, seed=0)
+    batches = synth.domain_batches(model, T)
+    results = {}
+    with open(path, "a") as f:
+        for name, doms in batches.items():
+            routing = []
+            for l in range(L):
+                ids, w = synth.domain_routing(model, subsets, doms, l, seed=0)
+                routing.append((torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda()))
+            ml.step(routing)
+            us = ml.unions()
+            ms = ml.time(steps, warmup, routing)
+            step_bytes = sum(layer_bytes(shape, T, u, False) for u in us)
+            rec = {"workload": "qwen3_30b_a3b x48 layers, T=128, domain-clustered", "batch": name,
+                   "step_ms": ms, "mean_union": float(np.mean(us)), "unions": us,
+                   "step_GBps": step_bytes / ms / 1e6}
+            results[name] = rec
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            log(f"domains {name}: {ms:.3f} ms/step, mean union {np.mean(us):.1f}, {rec['step_GBps']:.0f} GB/s")
+        same = [results[k] for k in results if k.startswith("same_")]
+        summary = {"workload": "qwen3_30b_a3b x48 layers, T=128, domain-clustered", "summary": True,
+                   "same_domain_mean_step_ms": float(np.mean([r["step_ms"] for r in same])),
+                   "same_domain_mean_union": float(np.mean([r["mean_union"] for r in same])),
+                   "mixed_step_ms": results["mixed"]["step_ms"],
+                   "mixed_mean_union": results["mixed"]["mean_union"]}
+        summary["union_reduction"] = 1 - summary["same_domain_mean_union"] / summary["mixed_mean_union"]
+        summary["step_time_reduction"] = 1 - summary["same_domain_mean_step_ms"] / summary["mixed_step_ms"]
+        f.write(json.dumps(summary) + "\n")
+        log(f"domains: same-domain batches use {100 * summary['union_reduction']:.1f}% fewer experts per layer "
+            f"and {100 * summary['step_time_reduction']:.1f}% less step time than the mixed batch")
+    del ml
+    torch.cuda.empty_cache()
+
+
+def gpt_oss_workload(path: str, steps: int, warmup: int, resident: int = 20) -> None:
+    """36 gpt-oss-120b-shaped layers per step (bf16), T=256, gate-routed and
+    controlled unions 32 and 128.  ``resident`` distinct layers are allocated
+    (6.37 GB each) and cycled."""
+    shape = synth.SHAPES["gpt_oss_120b"]
+    L, T = 36, 256
+    ml = MultiLayer(shape, T, L, resident)
+    with open(path, "a") as f:
+        for U in (None, 32, 128):
+            routing = None
+            if U is not None:
+                routing = []
+                for l in range(L):
+                    ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0, layer=l)
+                    routing.append((torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda()))
+            ml.step(routing)
+            us = ml.unions()
+            ms = ml.time(steps, warmup, routing)
+            step_bytes = sum(layer_bytes(shape, T, u, routing is None) for u in us)
+            rec = {"workload": f"gpt_oss_120b x{L} layers ({resident} resident, cycled), T=256",
+                   "routing": "gate" if U is None else f"controlled U={U}", "step_ms": ms,
+                   "mean_union": float(np.mean(us)), "step_GBps": step_bytes / ms / 1e6}
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            log(f"gpt-oss {rec['routing']}: {ms:.3f} ms/step, mean union {rec['mean_union']:.1f}, "
+                f"{rec['step_GBps']:.0f} GB/s")
+    del ml
+    torch.cuda.empty_cache()
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +370,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="host time budget of the CPU-oracle baseline (0 to skip)")
     ap.add_argument("--sweep", default="", help="also write the union and batch sweeps to this file")
+    ap.add_argument("--multilayer", default="",
+                    help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
+                         "appending JSON lines to this file")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -295,6 +426,9 @@ def main() -> int:
     torch.cuda.empty_cache()
     if args.sweep:
         sweep(args.sweep, max(20, args.steps // 2), args.warmup)
+    if args.multilayer:
+        domain_workload(args.multilayer, 10, 2)
+        gpt_oss_workload(args.multilayer, 5, 1)
     print(json.dumps(out), flush=True)
     return 0
 
