@@ -49,14 +49,31 @@ __host__ __device__ constexpr int ring_depth() {
   return NT <= 2 ? ELDR_FFN_RING_SMALL : ELDR_FFN_RING_LARGE;
 }
 
-// Bytes of one LDS staging buffer (two are used, double-buffered): at least
-// a base size, and always room for a chunk of ring_depth k-steps of the
-// largest pass (NT * 16 tokens, 128 bytes per k-step, 16 bytes of padding).
+// k-steps per staged chunk: a whole number of ring cycles, as many as keep
+// one chunk of NT * 16 tokens within about 33 KB of LDS.
+#ifndef ELDR_FFN_CYCLES1
+#define ELDR_FFN_CYCLES1 2
+#endif
+#ifndef ELDR_FFN_CYCLES2
+#define ELDR_FFN_CYCLES2 1
+#endif
+template <int NT>
+__host__ __device__ constexpr int chunk_steps() {
+  return ring_depth<NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
+}
+
+#ifndef ELDR_FFN_MAX_CHUNK
+#define ELDR_FFN_MAX_CHUNK 8
+#endif
+// Longest chunk of any pass shape (a chunk's k-steps are unrolled).
+constexpr int kMaxChunk = ELDR_FFN_MAX_CHUNK;
+__host__ __device__ constexpr int min_c(int a, int b) { return a < b ? a : b; }
+
+// Bytes of one LDS staging buffer (two are used, double-buffered): NT * 16
+// token rows of chunk_steps k-steps (128 bytes each) plus 16 bytes of padding.
 template <int NT>
 __host__ __device__ constexpr int lds_buf_bytes() {
-  constexpr int base = NT == 1 ? 16 * 1024 : NT == 2 ? 24 * 1024 : 34 * 1024;
-  constexpr int need = NT * 16 * (128 * ring_depth<NT>() + 16);
-  return base > need ? base : ((need + 1023) / 1024) * 1024;
+  return NT * 16 * (128 * chunk_steps<NT>() + 16);
 }
 
 enum FfnMode { kUp = 0, kDown = 1 };
@@ -82,11 +99,11 @@ __host__ __device__ constexpr int rows_per_block() {
   return MODE == kUp ? kFfnWaves * 16 : kFfnWaves * 32;
 }
 
-// LDS layout of one staged chunk: per token a row of kcs k-steps; each
-// k-step holds 4 groups of 8 k-values; each group is 8 bf16 high parts then
-// 8 bf16 low parts (32 bytes).  Row stride = 128 * kcs + 16 bytes, an odd
-// multiple of 16, so the 16 lanes that read 16 tokens hit distinct banks.
-__device__ __forceinline__ int lds_stride(int kcs) { return 128 * kcs + 16; }
+// LDS layout of one staged chunk: per token a row of the chunk's k-steps;
+// each k-step holds 4 groups of 8 k-values; each group is 8 bf16 high parts
+// then 8 bf16 low parts (32 bytes).  The row stride is 128 bytes per k-step
+// plus 16, an odd multiple of 16, so the 16 lanes that read 16 tokens hit
+// distinct banks.
 
 template <int N>
 struct Int {
@@ -137,8 +154,6 @@ template <int MODE, int NT>
 __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   constexpr int kBuf = lds_buf_bytes<NT>();
   constexpr int kRing = ring_depth<NT>();
-  static_assert(kBuf >= NT * 16 * (128 * kRing + 16), "a chunk of kRing k-steps must fit");
-  constexpr int kGroups = (kBuf / 32 + kFfnThreads - 1) / kFfnThreads;  // staged groups per thread
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
   __shared__ int tok[NT * 16];
 
@@ -197,45 +212,60 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   for (int p0 = 0; p0 < c_total; p0 += NT * 16) {
     const int c = min(NT * 16, c_total - p0);
     const int nt = (c + 15) / 16;
-    // k-steps per staged chunk: a multiple of kRing that fits c token rows.
-    const int kcs = max(kRing, (((kBuf / c - 16) / 128) / kRing) * kRing);
-    const int stride = lds_stride(kcs);
 
     __syncthreads();  // the previous pass has finished with LDS
     if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
     __syncthreads();
 
-    // Fetch this thread's share of chunk [ks, ks + klen) k-steps into
-    // registers.  Every thread issues the same loads (a thread with no group
-    // left re-reads group 0), so the number of loads in flight is the same on
-    // every path and the compiler never has to drain the weight ring.
-    const size_t row_groups = (size_t)K / 8;  // 32-byte groups per activation row
-    u32x4 stg[kGroups][2];
-    auto fetch = [&](int ks, int klen) {
-      const int gpr = 4 * klen;
-      const int ng = c * gpr;
-#pragma unroll
-      for (int j = 0; j < kGroups; ++j) {
-        int q = tid + kFfnThreads * j;
-        q = q < ng ? q : 0;
-        const int n = q / gpr;
-        const int gi = q - n * gpr;
-        const u32x4* p =
-            reinterpret_cast<const u32x4*>(a.src) + 2 * ((size_t)tok[n] * row_groups + ks * 4 + gi);
-        stg[j][0] = p[0];
-        stg[j][1] = p[1];
-      }
-    };
-    auto publish = [&](int buf, int klen) {
-      const int gpr = 4 * klen;
-      const int ng = c * gpr;
-#pragma unroll
-      for (int j = 0; j < kGroups; ++j) {
+    // Pass shape: NTB token tiles, the LDS buffer split into token rows of
+    // kChunk k-steps -- fewer tokens, longer chunks, so every shape fills the
+    // same buffer and a small bucket crosses as few barriers as a large one.
+    auto run_pass = [&](auto NTB_) {
+      constexpr int NTB = decltype(NTB_)::value;
+      constexpr int kChunk = min_c(chunk_steps<NT>() * NT / NTB, kMaxChunk);
+      constexpr int kStride = 128 * kChunk + 16;  // bytes per staged token row: an odd multiple of 16
+      static_assert(kChunk % kRing == 0, "a chunk is a whole number of ring cycles");
+      static_assert(NTB * 16 * kStride <= kBuf, "a chunk fits its buffer");
+      constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
+      static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
+
+      // Activations are staged in chunks of kChunk k-steps.  Every chunk has
+      // the same shape, so the groups a thread moves, their LDS places and the
+      // number of loads issued between a chunk's fetch and its publish are
+      // compile-time constants: the compiler then waits only for the staged
+      // groups at a publish, never for the weights in flight behind them.
+      // Group q of a chunk is token row q / (4 kChunk), 32-byte group
+      // q % (4 kChunk); groups past the bucket or past the last k-step re-read
+      // group 0 of the chunk.
+      const size_t row_groups = (size_t)K / 8;  // 32-byte groups per activation row
+      u32x4 stg[kGroups][2];
+      auto group_ok = [&](int j, int ks) {
         const int q = tid + kFfnThreads * j;
-        if (q < ng) {
-          const int n = q / gpr;
-          const int gi = q - n * gpr;
-          u32x4* d = reinterpret_cast<u32x4*>(&lds[buf][n * stride + gi * 32]);
+        return q / (4 * kChunk) < c && ks * 4 + q % (4 * kChunk) < 4 * nk;
+      };
+      auto fetch = [&](int ks) {
+  #pragma unroll
+        for (int j = 0; j < kGroups; ++j) {
+          const int q = tid + kFfnThreads * j;
+          const bool ok = group_ok(j, ks);
+          const int n = ok ? q / (4 * kChunk) : 0;
+          const int gi = ok ? q % (4 * kChunk) : 0;
+          const u32x4* p =
+              reinterpret_cast<const u32x4*>(a.src) + 2 * ((size_t)tok[n] * row_groups + ks * 4 + gi);
+          stg[j][0] = p[0];
+          stg[j][1] = p[1];
+        }
+      };
+      // Every group is written, valid or not: the places of invalid groups
+      // (token rows >= c, k-steps past the end) lie inside the buffer and are
+      // never read, and unconditional stores keep every path's wait the same.
+      auto publish = [&](int buf) {
+  #pragma unroll
+        for (int j = 0; j < kGroups; ++j) {
+          const int q = tid + kFfnThreads * j;
+          const int n = q / (4 * kChunk);
+          const int gi = q % (4 * kChunk);
+          u32x4* d = reinterpret_cast<u32x4*>(&lds[buf][n * kStride + gi * 32]);
           if (MODE == kUp) {
             u32x4 hi, lo;
             split8_pk(stg[j][0], stg[j][1], hi, lo);
@@ -246,102 +276,119 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
             d[1] = stg[j][1];
           }
         }
+      };
+
+      f32x4 acc0[NTB], acc1[NTB];
+  #pragma unroll
+      for (int t = 0; t < NTB; ++t) {
+        acc0[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-    };
 
-    f32x4 acc0[NT], acc1[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      acc0[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+      ring_prologue();
 
-    ring_prologue();
-
-    // One k-step: multiply ring slot I against the staged tokens of
-    // chunk-relative step s - ks, then refill the slot with step s + kRing.
-    // The refill is issued after the MFMAs that read the slot, into the same
-    // registers, and a scheduling barrier keeps it there, so each slot stays
-    // in place and kRing steps of loads are always in flight.
-    auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
-      constexpr int i = decltype(I)::value;
-      const unsigned char* bs = bb + (s - ks) * 128;
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        if (t < nt) {
-          // Column n of the product depends only on column n of B, so lanes
-          // past the bucket read its last token and their columns are
-          // simply not stored.
-          const int n = min(t * 16 + arow, c - 1);
-          const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * stride);
-          const u32x4 bh = bp[0];
-          const u32x4 bl = bp[1];
-          acc0[t] = mfma16x16x32(ring0[i], bh, acc0[t]);
-          acc0[t] = mfma16x16x32(ring0[i], bl, acc0[t]);
-          acc1[t] = mfma16x16x32(ring1[i], bh, acc1[t]);
-          acc1[t] = mfma16x16x32(ring1[i], bl, acc1[t]);
+      // One k-step: multiply ring slot I against the staged tokens of
+      // chunk-relative step s - ks, then refill the slot with step s + kRing.
+      // The refill is issued after the MFMAs that read the slot, into the same
+      // registers, and a scheduling barrier keeps it there, so each slot stays
+      // in place and kRing steps of loads are always in flight.
+      auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
+        constexpr int i = decltype(I)::value % kRing;
+        const unsigned char* bs = bb + (s - ks) * 128;
+  #pragma unroll
+        for (int t = 0; t < NTB; ++t) {
+          if (t < nt) {
+            // Column n of the product depends only on column n of B, so lanes
+            // past the bucket read its last token and their columns are
+            // simply not stored.
+            const int n = min(t * 16 + arow, c - 1);
+            const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * kStride);
+            const u32x4 bh = bp[0];
+            const u32x4 bl = bp[1];
+            acc0[t] = mfma16x16x32(ring0[i], bh, acc0[t]);
+            acc0[t] = mfma16x16x32(ring0[i], bl, acc0[t]);
+            acc1[t] = mfma16x16x32(ring1[i], bh, acc1[t]);
+            acc1[t] = mfma16x16x32(ring1[i], bl, acc1[t]);
+          }
         }
-      }
-      const int sn = min(s + kRing, nk - 1);
-      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)sn * kFragElems);
-      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)sn * kFragElems);
-      __builtin_amdgcn_sched_barrier(0);
-    };
+        const int sn = min(s + kRing, nk - 1);
+        ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)sn * kFragElems);
+        ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)sn * kFragElems);
+        __builtin_amdgcn_sched_barrier(0);
+      };
 
-    fetch(0, min(kcs, nk));
-    for (int ks = 0, chunk = 0; ks < nk; ks += kcs, ++chunk) {
-      const int ke = min(nk, ks + kcs);
-      const int buf = chunk & 1;
-      // Buffer `buf` was last read two chunks ago; every wave has passed the
-      // barrier of the previous chunk since, so it is free to overwrite.
-      publish(buf, ke - ks);
+      // Chunk 0 is staged before the loop.  Each iteration then fetches the
+      // next chunk (always issued: the last full chunk fetches the tail chunk,
+      // or itself again), runs kChunk k-steps, unrolled, and publishes the next
+      // chunk into the other buffer.  In steady state the staged groups are
+      // older than the weight loads behind them, so a publish waits for them
+      // alone.  Chunk starts are multiples of kRing, so step ks + I sits in
+      // ring slot I % kRing.  The buffer published at the end of iteration ch
+      // was last read in iteration ch - 1, before the previous barrier.
+      const int nfull = nk / kChunk;
+      const int last_start = ((nk - 1) / kChunk) * kChunk;
+      fetch(0);
+      publish(0);
       __syncthreads();
-      if (ke < nk) fetch(ke, min(kcs, nk - ke));
-
-      const unsigned char* bb = &lds[buf][kgrp * 32];
-      // ks is a multiple of kRing, so slot i always holds step sb + i.
-      const int kfull = ks + ((ke - ks) / kRing) * kRing;
-      for (int sb = ks; sb < kfull; sb += kRing) {
-        static_for<kRing>([&](auto I) { kstep(I, sb + decltype(I)::value, bb, ks); });
+      for (int ch = 0; ch < nfull; ++ch) {
+        const int ks = ch * kChunk;
+        const int next = min(ks + kChunk, last_start);
+        fetch(next);
+        const unsigned char* bb = &lds[ch & 1][kgrp * 32];
+        static_for<kChunk>([&](auto I) { kstep(I, ks + decltype(I)::value, bb, ks); });
+        publish((ch + 1) & 1);
+        __syncthreads();
       }
-      // Tail (only in the last chunk, when nk is not a multiple of kRing).
-      if (kfull < ke) {
-        static_for<kRing>([&](auto I) {
-          if (kfull + decltype(I)::value < ke) kstep(I, kfull + decltype(I)::value, bb, ks);
+      // Tail chunk (when nk is not a multiple of kChunk), already staged.
+      if (nfull * kChunk < nk) {
+        const int ks = nfull * kChunk;
+        const unsigned char* bb = &lds[nfull & 1][kgrp * 32];
+        static_for<kChunk>([&](auto I) {
+          if (ks + decltype(I)::value < nk) kstep(I, ks + decltype(I)::value, bb, ks);
         });
       }
-    }
 
-    // ---- epilogue: lane holds rows r0 + 4 * (lane / 16) + i of token lane % 16
-    const int rsub = 4 * kgrp;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int n = t * 16 + arow;
-      if (t < nt && n < c) {
-        const size_t sl = (size_t)(s_begin + p0 + n);
-        if (MODE == kUp) {
-          if (ok0) {
-            // h for rows r0 + rsub .. + 3: half of one 8-value group of the
-            // split layout (high parts at +0, low parts at +16 bytes).
-            uint32_t hi[4], lo[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) split_bf16(silu(acc0[t][i]) * acc1[t][i], hi[i], lo[i]);
-            const int col = r0 + rsub;
-            unsigned char* row = static_cast<unsigned char*>(a.dst) + sl * (size_t)a.rows * 4;
-            unsigned char* grp = row + (col / 8) * 32 + (col % 8) * 2;
-            *reinterpret_cast<uint2*>(grp) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
-            *reinterpret_cast<uint2*>(grp + 16) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+      // ---- epilogue: lane holds rows r0 + 4 * (lane / 16) + i of token lane % 16
+      const int rsub = 4 * kgrp;
+  #pragma unroll
+      for (int t = 0; t < NTB; ++t) {
+        const int n = t * 16 + arow;
+        if (t < nt && n < c) {
+          const size_t sl = (size_t)(s_begin + p0 + n);
+          if (MODE == kUp) {
+            if (ok0) {
+              // h for rows r0 + rsub .. + 3: half of one 8-value group of the
+              // split layout (high parts at +0, low parts at +16 bytes).
+              uint32_t hi[4], lo[4];
+  #pragma unroll
+              for (int i = 0; i < 4; ++i) split_bf16(silu(acc0[t][i]) * acc1[t][i], hi[i], lo[i]);
+              const int col = r0 + rsub;
+              unsigned char* row = static_cast<unsigned char*>(a.dst) + sl * (size_t)a.rows * 4;
+              unsigned char* grp = row + (col / 8) * 32 + (col % 8) * 2;
+              *reinterpret_cast<uint2*>(grp) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+              *reinterpret_cast<uint2*>(grp + 16) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+            }
+          } else {
+            float* y = static_cast<float*>(a.dst) + sl * a.rows;
+            if (ok0)
+              *reinterpret_cast<float4*>(y + r0 + rsub) =
+                  make_float4(acc0[t][0], acc0[t][1], acc0[t][2], acc0[t][3]);
+            if (ok1)
+              *reinterpret_cast<float4*>(y + r0 + 16 + rsub) =
+                  make_float4(acc1[t][0], acc1[t][1], acc1[t][2], acc1[t][3]);
           }
-        } else {
-          float* y = static_cast<float*>(a.dst) + sl * a.rows;
-          if (ok0)
-            *reinterpret_cast<float4*>(y + r0 + rsub) =
-                make_float4(acc0[t][0], acc0[t][1], acc0[t][2], acc0[t][3]);
-          if (ok1)
-            *reinterpret_cast<float4*>(y + r0 + 16 + rsub) =
-                make_float4(acc1[t][0], acc1[t][1], acc1[t][2], acc1[t][3]);
         }
       }
+    };
+    if constexpr (NT == 1) {
+      run_pass(Int<1>{});
+    } else if constexpr (NT == 2) {
+      if (nt == 1) run_pass(Int<1>{});
+      else run_pass(Int<2>{});
+    } else {
+      if (nt == 1) run_pass(Int<1>{});
+      else if (nt == 2) run_pass(Int<2>{});
+      else run_pass(Int<NT>{});
     }
   }
 }
