@@ -41,7 +41,8 @@ constexpr int kFfnThreads = 256;  // 4 waves
 constexpr int kFfnWaves = kFfnThreads / kWave;
 constexpr int kKStep = 32;        // k per MFMA
 constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
-constexpr int kMaxTiles = 4;      // token tiles of 16 per pass: at most 64 tokens per pass
+constexpr int kMaxTiles = 4;      // token tiles of 16 per item: at most 64 tokens of an expert
+constexpr int kMaxExpertsPerXcd = (MOE_MAX_E + kNumXcd - 1) / kNumXcd;
 
 // k-steps of weights in flight per wave (the prefetch depth of the ring).
 template <int NT>
@@ -89,7 +90,10 @@ struct FfnArgs {
   void* dst;                   // up: h [T*K, I] as bf16 pairs; down: y_perm [T*K, H] fp32
   int rows;                    // output rows per expert: up I, down H
   int kdim;                    // reduction length: up H, down I
-  int tiles;                   // workgroups per expert
+  int tiles;                   // row bands per expert
+  int extra_groups;            // MULTI: slots per XCD beyond one group per expert, in bands
+  int max_groups;              // MULTI: token groups of the largest possible bucket (T)
+  int experts;                 // E
 };
 
 // Rows per workgroup: up -> 4 waves x 16 rows (each wave reads the same 16
@@ -150,70 +154,75 @@ __device__ __forceinline__ void split8_pk(const u32x4& a, const u32x4& b, u32x4&
 // from fp32 and splits it on the way into LDS; its epilogue writes h already
 // split, so the down kernel stages h with a plain copy.
 
-template <int MODE, int NT>
+template <int MODE, int NT, bool MULTI>
 __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
   constexpr int kBuf = lds_buf_bytes<NT>();
   constexpr int kRing = ring_depth<NT>();
+  constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
-  __shared__ int tok[NT * 16];
+  __shared__ int tok[kGroupTokens];
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave;
 
-  // ---- which (expert, row band) this workgroup owns -----------------------
-  const int bid = blockIdx.x;
-  const int xcd = bid % kNumXcd;
-  const int slot = bid / kNumXcd;
-  const int u = (slot / a.tiles) * kNumXcd + xcd;
-  const int tile = slot % a.tiles;
-  const int U = *a.union_size;
-  if (u >= U) return;  // also covers U < 0 (invalid routing)
-  const int e = a.union_ids[u];
-  const int s_begin = a.offsets[e];
-  const int c_total = a.offsets[e + 1] - s_begin;
-  if (c_total <= 0) return;
-
+  // ---- work items -----------------------------------------------------------
+  // Expert u of the union belongs to XCD u % 8 (workgroups are dealt to the
+  // XCDs round-robin, so workgroup b runs on XCD b % 8 and is that XCD's
+  // slot b / 8).  An item is (expert, row band, token group of up to
+  // kGroupTokens tokens); an XCD's items are numbered expert by expert, and
+  // within an expert band by band with the band's token groups adjacent, so
+  // the workgroups that read one band's weights for different tokens run
+  // side by side and share the XCD's L2.  A slot takes items slot,
+  // slot + slots, ... .  Without MULTI (batches of at most kGroupTokens
+  // tokens) every expert has one group; with it, the group counts of this
+  // XCD's experts are read and prefix-summed first.
+  const int xcd = blockIdx.x % kNumXcd;
+  const int slot = blockIdx.x / kNumXcd;
+  const int slots = gridDim.x / kNumXcd;
   const int K = a.kdim;
   const int nk = K / kKStep;
-  const int r0 = tile * rows_per_block<MODE>() + wave * (MODE == kUp ? 16 : 32);
-  const bool ok0 = r0 < a.rows;
-  const bool ok1 = MODE == kUp ? ok0 : (r0 + 16 < a.rows);
-  // A 16-row tile past the end of the matrix (only when rows is not a
-  // multiple of the band) re-reads the band's first tile and is not stored.
-  const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE>();
-  const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE>());
-
-  // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
-  // (lane / 16).  Weights are packed (moe_pack_weights): the 64 lane pieces of
-  // one tile and k-step are a contiguous 1 KB fragment, and a tile's k-steps
-  // follow each other, so step s of a tile is at tile_base + s * 512 values.
   const int arow = lane & 15;
   const int kgrp = lane >> 4;
   const size_t tiles_per_expert = (size_t)(a.rows / 16);
-  const uint16_t* pa0 =
-      a.wa + ((e * tiles_per_expert + ra0 / 16) * nk) * kFragElems + lane * 8;
-  const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) +
-                        ((e * tiles_per_expert + ra1 / 16) * nk) * kFragElems + lane * 8;
 
-  // Weight ring: slot i holds the fragments of the k-step congruent to i
-  // mod kRing.  Loads past the last k-step re-read the last one (always
-  // issued, never used), which keeps the loop free of branches.
-  u32x4 ring0[kRing], ring1[kRing];
-  auto ring_prologue = [&]() {
-#pragma unroll
-    for (int i = 0; i < kRing; ++i) {
-      const int si = min(i, nk - 1);
-      ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)si * kFragElems);
-      ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)si * kFragElems);
-    }
-  };
-
-  for (int p0 = 0; p0 < c_total; p0 += NT * 16) {
-    const int c = min(NT * 16, c_total - p0);
+  // One item: the token group of up to kGroupTokens tokens starting at slot
+  // s_begin + p0 of expert e's bucket, against row band `tile`.
+  auto run_item = [&](const int e, const int tile, const int s_begin, const int p0, const int c) {
     const int nt = (c + 15) / 16;
 
-    __syncthreads();  // the previous pass has finished with LDS
+    const int r0 = tile * rows_per_block<MODE>() + wave * (MODE == kUp ? 16 : 32);
+    const bool ok0 = r0 < a.rows;
+    const bool ok1 = MODE == kUp ? ok0 : (r0 + 16 < a.rows);
+    // A 16-row tile past the end of the matrix (only when rows is not a
+    // multiple of the band) re-reads the band's first tile and is not stored.
+    const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE>();
+    const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE>());
+
+    // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
+    // (lane / 16).  Weights are packed (moe_pack_weights): the 64 lane pieces
+    // of one tile and k-step are a contiguous 1 KB fragment, and a tile's
+    // k-steps follow each other, so step s of a tile is at tile_base + s * 512.
+    const uint16_t* pa0 =
+        a.wa + ((e * tiles_per_expert + ra0 / 16) * nk) * kFragElems + lane * 8;
+    const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) +
+                          ((e * tiles_per_expert + ra1 / 16) * nk) * kFragElems + lane * 8;
+
+    // Weight ring: slot i holds the fragments of the k-step congruent to i
+    // mod kRing.  Loads past the last k-step re-read the last one (always
+    // issued, never used), which keeps the loop free of branches.
+    u32x4 ring0[kRing], ring1[kRing];
+    auto ring_prologue = [&]() {
+#pragma unroll
+      for (int i = 0; i < kRing; ++i) {
+        const int si = min(i, nk - 1);
+        ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)si * kFragElems);
+        ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)si * kFragElems);
+      }
+    };
+
+    ring_prologue();
+    __syncthreads();  // the previous item has finished with LDS
     if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
     __syncthreads();
 
@@ -284,8 +293,6 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
         acc0[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-
-      ring_prologue();
 
       // One k-step: multiply ring slot I against the staged tokens of
       // chunk-relative step s - ks, then refill the slot with step s + kRing.
@@ -390,29 +397,97 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
       else if (nt == 2) run_pass(Int<2>{});
       else run_pass(Int<NT>{});
     }
+  };
+
+  if constexpr (!MULTI) {
+    // At most kGroupTokens tokens per expert: slot = (expert / 8) * tiles + band.
+    const int u = (slot / a.tiles) * kNumXcd + xcd;
+    const int U = *a.union_size;
+    if (u >= U) return;  // also covers U < 0 (invalid routing)
+    const int e = a.union_ids[u];
+    if (e < 0 || e >= a.experts) return;  // not reached for a union member
+    const int s_begin = a.offsets[e];
+    const int c = a.offsets[e + 1] - s_begin;
+    if (c > 0) run_item(e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
+  } else {
+    // Every wave builds the table of its XCD's experts in registers: lane m
+    // holds expert m's id (union_ids is read together with union_size; it is
+    // -1 past the union), bucket start and size, its number of token groups,
+    // and the inclusive prefix sum of group counts.  An item is found with
+    // one ballot, and its expert's data with lane reads.
+    const int u_lane = xcd + kNumXcd * lane;
+    int e_lane = -1;
+    if (lane < kMaxExpertsPerXcd && u_lane < a.experts) e_lane = a.union_ids[u_lane];
+    const int U = *a.union_size;
+    if (U <= xcd) return;  // no expert on this XCD; also covers U < 0 (invalid routing)
+    const int M = (U - xcd + kNumXcd - 1) / kNumXcd;  // experts on this XCD
+    // An expert has at most max_groups token groups: slots past that bound
+    // leave before reading any bucket.
+    if (slot >= M * a.tiles * a.max_groups) return;
+    const bool member = lane < M && e_lane >= 0 && e_lane < a.experts;
+    int sb_lane = 0, c_lane = 0;
+    if (member) {
+      sb_lane = a.offsets[e_lane];
+      c_lane = a.offsets[e_lane + 1] - sb_lane;
+    }
+    const int g_lane = member ? (c_lane + kGroupTokens - 1) / kGroupTokens : 0;
+    int incl = g_lane;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    const int items = __builtin_amdgcn_readlane(incl, kWave - 1) * a.tiles;
+    for (int item = slot; item < items; item += slots) {
+      // m = number of experts whose items all precede this one
+      const int m = __popcll(__ballot(incl * a.tiles <= item));
+      const int g = __builtin_amdgcn_readlane(g_lane, m);
+      const int r = item - __builtin_amdgcn_readlane(incl - g_lane, m) * a.tiles;
+      const int tile = r / g;
+      const int group = r - tile * g;
+      const int p0 = group * kGroupTokens;
+      const int c = min(kGroupTokens, __builtin_amdgcn_readlane(c_lane, m) - p0);
+      if (c > 0)
+        run_item(__builtin_amdgcn_readlane(e_lane, m), tile,
+                 __builtin_amdgcn_readlane(sb_lane, m), p0, c);
+    }
   }
 }
 
+// Slots per XCD: one item per (expert, band) of the XCD's experts; batches
+// with more tokens than one item takes also get room for the average number
+// of extra token groups an XCD sees (T*K / (NT*16) extra groups at most in
+// all), and slots loop over any items beyond that.
 template <int MODE, int NT>
-static void launch_ffn(const FfnArgs& a, int E, hipStream_t s) {
-  const int groups = (E + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(kNumXcd * a.tiles * groups);
-  hipLaunchKernelGGL((ffn_kernel<MODE, NT>), grid, dim3(kFfnThreads), 0, s, a);
+static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
+  const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
+  if (T <= NT * 16) {
+    a.extra_groups = 0;
+    hipLaunchKernelGGL((ffn_kernel<MODE, NT, false>), dim3(kNumXcd * a.tiles * per_xcd),
+                       dim3(kFfnThreads), 0, s, a);
+  } else {
+    const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
+    a.extra_groups = extra;
+    a.max_groups = (T + NT * 16 - 1) / (NT * 16);
+    hipLaunchKernelGGL((ffn_kernel<MODE, NT, true>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
+                       dim3(kFfnThreads), 0, s, a);
+  }
 }
 
-// Token tiles held per pass: enough for every bucket when T is small (a
+// Token tiles of 16 per item: enough for every bucket when T is small (a
 // bucket never exceeds T tokens), at most kMaxTiles.
 template <int MODE>
-static void launch_ffn_nt(const FfnArgs& a, int T, int E, hipStream_t s) {
+static void launch_ffn_nt(const FfnArgs& a, int T, int K, int E, hipStream_t s) {
+  int nt_T = T;
 #ifdef ELDR_FFN_FORCE_NT
-  T = 16 * ELDR_FFN_FORCE_NT;
+  nt_T = 16 * ELDR_FFN_FORCE_NT;
 #endif
-  if (T <= 16)
-    launch_ffn<MODE, 1>(a, E, s);
-  else if (T <= 32)
-    launch_ffn<MODE, 2>(a, E, s);
+  if (nt_T <= 16)
+    launch_ffn<MODE, 1>(a, T, K, E, s);
+  else if (nt_T <= 32)
+    launch_ffn<MODE, 2>(a, T, K, E, s);
   else
-    launch_ffn<MODE, kMaxTiles>(a, E, s);
+    launch_ffn<MODE, kMaxTiles>(a, T, K, E, s);
 }
 
 }  // namespace eldr
@@ -451,9 +526,9 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint1
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w1, w3, offsets, perm_token, union_ids,
-                   union_size, ws, d.I, d.H, 0};
+                   union_size, ws, d.I, d.H, 0, 0, 1, d.E};
   up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
-  eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.E, s);
+  eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.K, d.E, s);
   return launch_status();
 }
 
@@ -471,10 +546,10 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, nullptr, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0};
+                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E};
   down.tiles =
       (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
-  eldr::launch_ffn_nt<eldr::kDown>(down, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  eldr::launch_ffn_nt<eldr::kDown>(down, d.T, d.K, d.E, reinterpret_cast<hipStream_t>(stream));
   return launch_status();
 }
 

@@ -88,14 +88,36 @@ def test_qwen_batch_sweep(T):
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
-def test_bucket_over_64_tokens_takes_passes():
-    # Every token picks the same 8 experts: 200 tokens per bucket, four passes.
+def test_bucket_over_64_tokens_takes_groups():
+    # Every token picks the same 8 experts: 200 tokens per bucket, four token groups.
     G.say("case: qwen layer, T=200, all tokens on experts 0..7 (buckets of 200)")
     layer = G.Layer(QWEN, 200)
     ids = np.tile(np.arange(8, dtype=np.int32), (200, 1))
     w = np.full((200, 8), 1 / 8, np.float32)
     g = layer.run(routing=(ids, w))
     assert g["union_size"] == 8
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+def test_heavy_experts_on_one_xcd():
+    # Union = experts 0..31; experts 0, 8, 16, 24 (union positions of one XCD)
+    # take every token, so that XCD has more (band, token group) items than
+    # workgroup slots and its slots loop.
+    shape = synth.LayerShape("heavy_xcd", E=32, K=8, H=512, I=256)
+    T = 512
+    G.say(f"case: E=32 top-8 H=512 I=256 T={T}, experts 0/8/16/24 take all {T} tokens")
+    rng = np.random.default_rng(11)
+    heavy = np.array([0, 8, 16, 24], np.int32)
+    light = np.setdiff1d(np.arange(32, dtype=np.int32), heavy)
+    ids = np.empty((T, 8), np.int32)
+    for t in range(T):
+        ids[t, :4] = heavy
+        ids[t, 4:] = rng.choice(light, 4, replace=False)
+    w = rng.dirichlet(np.ones(8), size=T).astype(np.float32)
+    layer = G.Layer(shape, T, seed=12)
+    g = layer.run(routing=(ids, w))
+    assert g["union_size"] == 32
+    assert g["counts"][heavy].tolist() == [T] * 4
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
