@@ -147,11 +147,11 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * s in [offsets[e], offsets[e+1]) holding token t = perm_token[s]:
  *   y_perm[s, :] = W2_e (silu(W1_e x[t]) * (W3_e x[t]))
  * Each active expert's weights are streamed from HBM once per call when it
- * has at most 64 tokens (a bigger bucket is processed in passes of 64 tokens,
- * each streaming the expert's rows again); experts outside the union are
- * never touched.
- * The grid is sized for E experts and reads union_size on the device, so no
- * host synchronisation is needed between moe_bucket and this call.
+ * has at most 64 tokens; a bigger bucket is split into groups of 64 tokens
+ * whose workgroups run side by side on one XCD and share that XCD's L2 for
+ * the repeated weight reads.  Experts outside the union are never touched.
+ * The grid is sized from E and T alone and reads union_size on the device,
+ * so no host synchronisation is needed between moe_bucket and this call.
  *
  * x [T, H] fp32; w1, w3 ([E, I, H]) and w2 ([E, H, I]) bf16 packed by
  * moe_pack_weights; offsets [E+1],

@@ -7,25 +7,31 @@
 //
 // * Two launches.  "up" computes h = silu(W1 x) * (W3 x) for every slot into
 //   the workspace (as bf16 pairs, see below); "down" computes y = W2 h.
-//   Within each launch a workgroup owns one expert and a band of output rows
-//   and streams that band's bf16 weights from HBM exactly once (128-bit loads
-//   straight into the MFMA A operand), for all of the expert's tokens at once.
+//   Within each launch a workgroup item is one expert, one band of output
+//   rows and up to 64 of the expert's tokens; it streams the band's bf16
+//   weights from HBM (128-bit loads straight into the MFMA A operand).
 //   Weights come packed by moe_pack_weights, so each load instruction reads
 //   one contiguous 1 KB MFMA fragment.
-// * The expert's tokens (at most 64 per pass) are gathered, carried as a pair
-//   of bf16 values (high part + rounded remainder) and staged in LDS in
-//   k-chunks, double-buffered, shared by the workgroup's four waves; each
-//   wave reads them as the MFMA B operand.  Tokens are padded to a multiple
-//   of 16 only in registers (lanes past the bucket repeat its last token and
-//   their output columns are not stored).
+// * An expert with at most 64 tokens has one item per band, so its weights
+//   are read once.  A bigger bucket is split into token groups of 64 whose
+//   items for one band get adjacent workgroup slots on one XCD: they run side
+//   by side and the second read of the band is served mostly by that XCD's
+//   L2 rather than HBM.
+// * The item's tokens are gathered, carried as a pair of bf16 values (high
+//   part + rounded remainder) and staged in LDS in fixed-shape chunks,
+//   double-buffered, shared by the workgroup's four waves; each wave reads
+//   them as the MFMA B operand.  Tokens are padded to a multiple of 16 only
+//   in registers (lanes past the bucket repeat its last token and their
+//   output columns are not stored).
 // * Each wave keeps a ring of weight fragments for the next k-steps in
-//   flight; a refill is issued right after the MFMAs that consumed its slot.
-// * The grid is sized for E experts; a workgroup reads the union size on the
-//   device and returns at once if its slot is past it, so inactive experts
+//   flight; a refill is issued right after the MFMAs that consumed its slot,
+//   and staging is arranged so that the compiler never has to drain the ring.
+// * The grid is sized from E (and T) alone; a workgroup reads the union size
+//   on the device and returns at once if it has no item, so inactive experts
 //   cost one scalar load and no host synchronisation is needed.
-// * Workgroups of one expert are placed on one XCD (the dispatcher deals
-//   workgroups round-robin over the 8 XCDs), so the expert's activations are
-//   read into a single L2.
+// * Experts of the union are dealt to XCDs round-robin (the dispatcher deals
+//   workgroups round-robin over the 8 XCDs), so all of an expert's
+//   workgroups share one L2 for its activations and weights.
 #include "common.hpp"
 
 namespace eldr {
