@@ -174,6 +174,38 @@ class Bench:
                 "up_ms_median": float(np.median(up)), "down_ms_median": float(np.median(down))}
 
 
+def calibration(reps: int = 10) -> dict:
+    """What plain streaming achieves on this GPU, for context beside the 8 TB/s peak:
+    torch.sum over a 2 GiB fp32 tensor (reads) and a 2 GiB device-to-device copy
+    (reads + writes), best of `reps`, HIP events on the current stream."""
+    n = (2 << 30) // 4
+    a = torch.ones(n, device="cuda")
+    b = torch.empty_like(a)
+    s = torch.zeros((), device="cuda")
+
+    def best(fn) -> float:
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1))
+        return min(t)
+
+    read_ms = best(lambda: torch.sum(a, out=s))
+    copy_ms = best(lambda: b.copy_(a))
+    del a, b
+    torch.cuda.empty_cache()
+    return {"stream_read_GBps": round(4 * n / read_ms / 1e6, 1),
+            "copy_GBps_read_plus_write": round(8 * n / copy_ms / 1e6, 1),
+            "how": "best of 10: torch.sum over a 2 GiB fp32 tensor; a 2 GiB device copy"}
+
+
 def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:
     """The float64 oracle on the host, one BLAS thread, on the same layer."""
     from threadpoolctl import threadpool_limits
@@ -419,6 +451,8 @@ def main() -> int:
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "bytes_per_launch": ub},
     }
+    out["calibration"] = calibration()
+    log(f"calibration: {out['calibration']}")
     if args.cpu_seconds > 0:
         log("timing the CPU oracle ...")
         out["cpu_baseline"] = cpu_baseline(bench, U, args.cpu_seconds)
