@@ -43,8 +43,12 @@ namespace eldr {
 #define ELDR_FFN_RING_LARGE 4
 #endif
 
-constexpr int kFfnThreads = 256;  // 4 waves
-constexpr int kFfnWaves = kFfnThreads / kWave;
+#ifndef ELDR_FFN_UP_WAVES
+#define ELDR_FFN_UP_WAVES 4
+#endif
+#ifndef ELDR_FFN_DOWN_WAVES
+#define ELDR_FFN_DOWN_WAVES 4
+#endif
 constexpr int kKStep = 32;        // k per MFMA
 constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
 constexpr int kMaxTiles = 4;      // token tiles of 16 per item: at most 64 tokens of an expert
@@ -85,6 +89,18 @@ __host__ __device__ constexpr int lds_buf_bytes() {
 
 enum FfnMode { kUp = 0, kDown = 1 };
 
+// Waves per workgroup: each wave owns 16 output rows (up: of W1 and of W3)
+// or 32 (down: two 16-row tiles of W2), and all of them share the staged
+// activations.
+template <int MODE>
+__host__ __device__ constexpr int ffn_waves() {
+  return MODE == kUp ? ELDR_FFN_UP_WAVES : ELDR_FFN_DOWN_WAVES;
+}
+template <int MODE>
+__host__ __device__ constexpr int ffn_threads() {
+  return ffn_waves<MODE>() * kWave;
+}
+
 struct FfnArgs {
   const uint4* src;            // up: x [T, H] fp32; down: h [T*K, I] as bf16 pairs
   const uint16_t* wa;          // up: W1 [E, I, H]; down: W2 [E, H, I]
@@ -102,11 +118,11 @@ struct FfnArgs {
   int experts;                 // E
 };
 
-// Rows per workgroup: up -> 4 waves x 16 rows (each wave reads the same 16
-// rows of W1 and of W3); down -> 4 waves x 32 rows of W2 (two 16-row tiles).
+// Rows per workgroup: up -> 16 rows per wave (each wave reads the same 16
+// rows of W1 and of W3); down -> 32 rows of W2 per wave (two 16-row tiles).
 template <int MODE>
 __host__ __device__ constexpr int rows_per_block() {
-  return MODE == kUp ? kFfnWaves * 16 : kFfnWaves * 32;
+  return MODE == kUp ? ffn_waves<MODE>() * 16 : ffn_waves<MODE>() * 32;
 }
 
 // LDS layout of one staged chunk: per token a row of the chunk's k-steps;
@@ -161,7 +177,8 @@ __device__ __forceinline__ void split8_pk(const u32x4& a, const u32x4& b, u32x4&
 // split, so the down kernel stages h with a plain copy.
 
 template <int MODE, int NT, bool MULTI>
-__global__ __launch_bounds__(kFfnThreads) void ffn_kernel(FfnArgs a) {
+__global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
+  constexpr int kFfnThreads = ffn_threads<MODE>();
   constexpr int kBuf = lds_buf_bytes<NT>();
   constexpr int kRing = ring_depth<NT>();
   constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
@@ -470,13 +487,13 @@ static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
   if (T <= NT * 16) {
     a.extra_groups = 0;
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, false>), dim3(kNumXcd * a.tiles * per_xcd),
-                       dim3(kFfnThreads), 0, s, a);
+                       dim3(ffn_threads<MODE>()), 0, s, a);
   } else {
     const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
     a.extra_groups = extra;
     a.max_groups = (T + NT * 16 - 1) / (NT * 16);
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, true>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
-                       dim3(kFfnThreads), 0, s, a);
+                       dim3(ffn_threads<MODE>()), 0, s, a);
   }
 }
 
