@@ -29,7 +29,8 @@ contiguous along the reduction axis):
 
 Routing generators (used when the gate is bypassed) return ``ids`` [T, K]
 int32 (distinct within a token) and ``weights`` [T, K] fp32 summing to one per
-token.
+token.  ``prefill_picks`` draws the picks of a prefill forward over many MoE
+layers, for the expert-signature cache.
 """
 from __future__ import annotations
 
@@ -46,6 +47,7 @@ _STREAM_X = 0
 _STREAM_GATE = 1
 _STREAM_EXPERTS = 2
 _STREAM_ROUTING = 3
+_STREAM_PREFILL = 4
 _N_STREAMS = 8
 
 
@@ -208,4 +210,27 @@ def domain_batches(model: DomainModel, T: int, seed: int = 0) -> dict[str, np.nd
         raise ValueError("T must be a multiple of the number of domains for the mixed batch")
     out = {f"same_{d}": np.full(T, d, dtype=np.int64) for d in range(model.n_domains)}
     out["mixed"] = np.repeat(np.arange(model.n_domains, dtype=np.int64), T // model.n_domains)
+    return out
+
+
+def prefill_picks(n_layers: int, T: int, E: int, K: int, seed: int = 0, skew: float = 0.0
+                  ) -> np.ndarray:
+    """Top-k picks of T prefill tokens at n_layers MoE layers, int32 [n_layers, T, K].
+
+    Each token's K picks at a layer are distinct.  skew = 0 draws them
+    uniformly; skew > 0 draws them from a Zipf(skew) popularity over a random
+    permutation of the experts per layer (a few experts are hot).
+    """
+    rng = _rng(seed, _STREAM_PREFILL, n_layers, T, E, K)
+    out = np.empty((n_layers, T, K), dtype=np.int32)
+    for layer in range(n_layers):
+        if skew > 0:
+            order = rng.permutation(E)
+            p = np.arange(1, E + 1, dtype=np.float64) ** (-skew)
+            p /= p.sum()
+        for t in range(T):
+            if skew > 0:
+                out[layer, t] = order[rng.choice(E, size=K, replace=False, p=p)]
+            else:
+                out[layer, t] = rng.choice(E, size=K, replace=False)
     return out
