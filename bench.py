@@ -394,6 +394,87 @@ def gpt_oss_workload(path: str, steps: int, warmup: int, resident: int = 20) -> 
     torch.cuda.empty_cache()
 
 
+def signature_workload(path: str, reps: int = 20) -> None:
+    """The expert-signature cache at the paper's largest shape (48 MoE layers,
+    E=128, top-8): capture of one 2048-token prefill forward into 16-token
+    blocks of a 4096-block cache, and the per-request sums of 64 requests of
+    64 blocks.  GPU times are graph replays; the oracle runs the same capture
+    and sums on one host thread."""
+    from oracle import signature as SO
+
+    L, E, K, T, BS, NB, R = 48, 128, 8, 2048, 16, 4096, 64
+    rng = np.random.default_rng(0)
+    ids_np = synth.prefill_picks(L, T, E, K, seed=0, skew=1.1)
+    table_np = rng.permutation(NB)[:T // BS].astype(np.int32)
+    tb_np = table_np[np.arange(T) // BS]
+    ids = torch.from_numpy(ids_np).cuda()
+    tb = torch.from_numpy(tb_np).cuda()
+    blocks = torch.from_numpy(table_np).cuda()
+    sig = torch.zeros((NB, L, E), dtype=torch.int8, device="cuda")
+    req_table = torch.from_numpy(rng.integers(0, NB, (R, 64)).astype(np.int32)).cuda()
+    req_n = torch.full((R,), 64, dtype=torch.int32, device="cuda")
+    out = torch.empty((R, L, E), dtype=torch.int32, device="cuda")
+
+    def timed(fn) -> float:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (10 * reps) * 1e3  # us per call
+
+    reset_us = timed(lambda: B.moe_sig_reset(blocks, sig))
+    pair_us = timed(lambda: (B.moe_sig_reset(blocks, sig), B.moe_sig_capture(ids, tb, 0, L, E, sig)))
+    capture_us = pair_us - reset_us
+    counts_us = timed(lambda: B.moe_sig_request_counts(sig, req_table, req_n, out))
+    picks = L * T * K
+    t0 = time.perf_counter()
+    ref, _ = SO.capture(SO.new_cache(NB, L, E), ids_np, tb_np)
+    cpu_capture_s = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    tabs = req_table.cpu().numpy()
+    for r in range(R):
+        SO.request_counts(ref, tabs[r])
+    cpu_counts_s = time.perf_counter() - t0
+    # correctness of what was timed
+    B.moe_sig_reset(blocks, sig)
+    B.moe_sig_capture(ids, tb, 0, L, E, sig)
+    torch.cuda.synchronize()
+    ok = bool(np.array_equal(sig.cpu().numpy().astype(np.int64), ref))
+    counts_bytes = R * 64 * L * E + 4 * R * L * E
+    recs = [
+        {"workload": "signature capture: 48 layers, E=128, top-8, one 2048-token prefill, 16-token blocks",
+         "call": "moe_sig_capture", "us": round(capture_us, 2), "picks": picks,
+         "Gpicks_per_s": round(picks / capture_us / 1e3, 2),
+         "cpu_oracle": {"us": round(cpu_capture_s * 1e6), "cores": 1}, "matches_oracle": ok},
+        {"workload": "signature sums: 64 requests x 64 blocks, 48 layers, E=128",
+         "call": "moe_sig_request_counts", "us": round(counts_us, 2),
+         "GBps": round(counts_bytes / counts_us / 1e3, 1),
+         "roofline": {"bound": "hbm", "achieved": round(counts_bytes / counts_us / 1e3, 1),
+                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                      "frac": round(counts_bytes / counts_us / 1e3 / HBM_PEAK_GBS, 4)},
+         "cpu_oracle": {"us": round(cpu_counts_s * 1e6), "cores": 1}},
+        {"workload": "signature reset: 128 blocks of 6 KiB", "call": "moe_sig_reset",
+         "us": round(reset_us, 2)},
+    ]
+    with open(path, "a") as f:
+        for rec in recs:
+            f.write(json.dumps(rec) + "\n")
+            log(f"signature {rec['call']}: {rec['us']} us")
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -402,6 +483,10 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="host time budget of the CPU-oracle baseline (0 to skip)")
     ap.add_argument("--sweep", default="", help="also write the union and batch sweeps to this file")
+    ap.add_argument("--signature", default="",
+                    help="also time the expert-signature cache calls, appending JSON lines to this file")
+    ap.add_argument("--signature-only", action="store_true",
+                    help="run only the --signature measurement (no layer bench line)")
     ap.add_argument("--multilayer", default="",
                     help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
                          "appending JSON lines to this file")
@@ -414,6 +499,9 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     B.load()
+    if args.signature_only:
+        signature_workload(args.signature or "signature.jsonl")
+        return 0
     shape = synth.SHAPES["qwen3_30b_a3b"]
     T = 64
     bench = Bench(shape, T)
@@ -460,6 +548,8 @@ def main() -> int:
     torch.cuda.empty_cache()
     if args.sweep:
         sweep(args.sweep, max(20, args.steps // 2), args.warmup)
+    if args.signature:
+        signature_workload(args.signature)
     if args.multilayer:
         domain_workload(args.multilayer, 10, 2)
         gpt_oss_workload(args.multilayer, 5, 1)

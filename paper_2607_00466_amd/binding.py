@@ -17,7 +17,9 @@ import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libeldr_moe.so")
-HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "eldr_moe.h")
+INCLUDE_DIR = os.path.join(os.path.dirname(_PKG), "include")
+HEADER_PATH = os.path.join(INCLUDE_DIR, "eldr_moe.h")
+HEADER_PATHS = (HEADER_PATH, os.path.join(INCLUDE_DIR, "eldr_signature.h"))
 
 MOE_OK = 0
 MOE_ERR_INVALID = -1
@@ -56,6 +58,9 @@ _SIGNATURES = {
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
     "moe_pack_weights": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
                                         _vp]),
+    "moe_sig_capture": (ctypes.c_int, [_vp, _vp] + [ctypes.c_int32] * 7 + [_vp, _vp, _vp]),
+    "moe_sig_reset": (ctypes.c_int, [_vp] + [ctypes.c_int32] * 4 + [_vp, _vp]),
+    "moe_sig_request_counts": (ctypes.c_int, [_vp, _vp, _vp] + [ctypes.c_int32] * 5 + [_vp, _vp]),
 }
 
 _lib = None
@@ -77,9 +82,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
-def header_functions(path: str = HEADER_PATH) -> list[str]:
-    """Names of the functions include/eldr_moe.h declares."""
-    text = open(path).read()
+def header_functions(paths=HEADER_PATHS) -> list[str]:
+    """Names of the functions the headers under include/ declare."""
+    text = "\n".join(open(p).read() for p in paths)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(moe_\w+)\s*\(", text, re.M)))
 
 
@@ -281,3 +286,48 @@ def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None
                    buf.y_perm, buf.ws, stream)
     moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
     return buf.out
+
+
+# ----------------------------------------------------------------------------- signature cache
+
+def moe_sig_capture(ids, token_block, layer0: int, L: int, E: int, sig, rejected=None,
+                    stream=None) -> None:
+    """Add one forward's picks ids [n_layers, T, K] to the int8 cache sig [num_blocks, L, E]."""
+    if ids.dim() != 3:
+        raise ValueError("ids: expected [n_layers, T, K]")
+    n_layers, T, K = ids.shape
+    if sig.dim() != 3 or tuple(sig.shape[1:]) != (L, E):
+        raise ValueError("sig: expected [num_blocks, L, E]")
+    _need(ids, "ids", torch.int32, n_layers * T * K)
+    _need(token_block, "token_block", torch.int32, T)
+    _need(sig, "sig", torch.int8, sig.numel())
+    if rejected is not None:
+        _need(rejected, "rejected", torch.int32, 1)
+    _check("moe_sig_capture", load().moe_sig_capture(
+        _ptr(ids), _ptr(token_block), n_layers, T, K, layer0, L, E, sig.shape[0], _ptr(sig),
+        _ptr(rejected), _stream(stream)))
+
+
+def moe_sig_reset(blocks, sig, stream=None) -> None:
+    """Zero the rows of the listed blocks of sig [num_blocks, L, E]."""
+    _need(blocks, "blocks", torch.int32, blocks.numel())
+    _need(sig, "sig", torch.int8, sig.numel())
+    nb, L, E = sig.shape
+    _check("moe_sig_reset", load().moe_sig_reset(_ptr(blocks), blocks.numel(), L, E, nb, _ptr(sig),
+                                                 _stream(stream)))
+
+
+def moe_sig_request_counts(sig, block_table, n_blocks, out=None, stream=None) -> torch.Tensor:
+    """Per-request sums of block rows: out [R, L, E] int32."""
+    nb, L, E = sig.shape
+    R, max_blocks = block_table.shape
+    _need(sig, "sig", torch.int8, sig.numel())
+    _need(block_table, "block_table", torch.int32, R * max_blocks)
+    _need(n_blocks, "n_blocks", torch.int32, R)
+    if out is None:
+        out = torch.empty((R, L, E), dtype=torch.int32, device=sig.device)
+    _need(out, "out", torch.int32, R * L * E)
+    _check("moe_sig_request_counts", load().moe_sig_request_counts(
+        _ptr(sig), _ptr(block_table), _ptr(n_blocks), R, max_blocks, L, E, nb, _ptr(out),
+        _stream(stream)))
+    return out

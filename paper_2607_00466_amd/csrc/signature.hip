@@ -1,0 +1,161 @@
+// The block-granular expert-signature cache (Design, Prefix Cache Coherence):
+// capture of a prefill forward's picks into int8 per-block rows, block reset,
+// and per-request sums over a block table.
+//
+// capture: one thread per (layer, token, pick).  Four int8 cells share one
+// 32-bit word, so a pick adds 1 << (8 * (cell % 4)) to its word with a 32-bit
+// device atomic.  A cell never exceeds 127 (a block holds at most 127 tokens
+// and a token picks an expert at most once per layer), so no carry crosses
+// into the neighbouring cell; integer atomics make the result independent of
+// the order of the picks.
+//
+// request counts: one thread per 4-cell word of a request's [L, E] row,
+// summing that word over the request's blocks (coalesced 32-bit loads of
+// consecutive words of each block's row) into four int32 counts.
+#include "common.hpp"
+#include "eldr_signature.h"
+
+namespace eldr {
+
+constexpr int kSigThreads = 256;
+
+__global__ __launch_bounds__(kSigThreads) void sig_capture_kernel(
+    const int32_t* __restrict__ ids, const int32_t* __restrict__ token_block, int64_t picks,
+    int T, int K, int layer0, int L, int E, int num_blocks, uint32_t* __restrict__ sig_words,
+    int32_t* __restrict__ rejected) {
+  const int64_t p = (int64_t)blockIdx.x * kSigThreads + threadIdx.x;  // (l * T + t) * K + j
+  bool bad = false;
+  if (p < picks) {
+    const int64_t lt = p / K;
+    const int t = (int)(lt % T);
+    const int l = (int)(lt / T);
+    const int b = token_block[t];
+    if (b >= 0) {
+      const int e = ids[p];
+      if (b >= num_blocks || e < 0 || e >= E) {
+        bad = true;
+      } else {
+        const int64_t cell = ((int64_t)b * L + layer0 + l) * E + e;
+        atomicAdd(&sig_words[cell >> 2], 1u << (8 * (int)(cell & 3)));
+      }
+    }
+  }
+  if (rejected) {
+    // one atomic per wave that saw a rejected pick
+    const uint64_t m = __ballot(bad);
+    if (m && (threadIdx.x % kWave) == 0) atomicAdd(rejected, (int)__popcll(m));
+  }
+}
+
+__global__ __launch_bounds__(kSigThreads) void sig_reset_kernel(const int32_t* __restrict__ blocks,
+                                                               int row_words, int num_blocks,
+                                                               uint32_t* __restrict__ sig_words) {
+  const int b = blocks[blockIdx.y];
+  if (b < 0 || b >= num_blocks) return;
+  const int w = blockIdx.x * kSigThreads + threadIdx.x;
+  if (w < row_words) sig_words[(int64_t)b * row_words + w] = 0u;
+}
+
+__global__ __launch_bounds__(kSigThreads) void sig_request_kernel(
+    const uint32_t* __restrict__ sig_words, const int32_t* __restrict__ block_table,
+    const int32_t* __restrict__ n_blocks, int max_blocks, int row_words, int num_blocks,
+    int4* __restrict__ out) {
+  const int r = blockIdx.y;
+  const int w = blockIdx.x * kSigThreads + threadIdx.x;
+  if (w >= row_words) return;
+  // An empty cache (num_blocks == 0, sig may be null) contributes nothing.
+  const int n = num_blocks > 0 ? min(max(n_blocks[r], 0), max_blocks) : 0;
+  const int32_t* table = block_table + (int64_t)r * max_blocks;
+  // Branch-free and unrolled, so a thread has several block loads in flight:
+  // an invalid block id reads block 0's word and adds nothing.
+  int4 acc = make_int4(0, 0, 0, 0);
+#pragma unroll 8
+  for (int i = 0; i < n; ++i) {
+    const int b = table[i];
+    const bool ok = b >= 0 && b < num_blocks;
+    const uint32_t v = sig_words[(int64_t)(ok ? b : 0) * row_words + w] & (ok ? 0xffffffffu : 0u);
+    // the four int8 cells of the word, sign-extended (cell 0 is the low byte)
+    acc.x += (int)(int8_t)(v & 0xffu);
+    acc.y += (int)(int8_t)((v >> 8) & 0xffu);
+    acc.z += (int)(int8_t)((v >> 16) & 0xffu);
+    acc.w += (int)(int8_t)(v >> 24);
+  }
+  out[(int64_t)r * row_words + w] = acc;
+}
+
+}  // namespace eldr
+
+namespace {
+
+int check_sig_shape(int32_t L, int32_t E, int32_t num_blocks) {
+  if (L <= 0 || E <= 0 || num_blocks < 0) return MOE_ERR_INVALID;
+  if (L > MOE_SIG_MAX_LAYERS || E > MOE_MAX_E) return MOE_ERR_UNSUPPORTED;
+  if (((int64_t)L * E) % 4 != 0) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_sig_capture(const int32_t* ids, const int32_t* token_block, int32_t n_layers,
+                               int32_t T, int32_t K, int32_t layer0, int32_t L, int32_t E,
+                               int32_t num_blocks, int8_t* sig, int32_t* rejected, void* stream) {
+  using namespace eldr_host;
+  int st = check_sig_shape(L, E, num_blocks);
+  if (st != MOE_OK) return st;
+  if (n_layers < 0 || T < 0 || K <= 0 || K > E || layer0 < 0 || layer0 + n_layers > L)
+    return MOE_ERR_INVALID;
+  if (T > MOE_SIG_MAX_TOKENS) return MOE_ERR_UNSUPPORTED;
+  const int64_t picks = (int64_t)n_layers * T * K;
+  if (picks == 0 || num_blocks == 0) return MOE_OK;
+  if (!ids || !token_block || !sig) return MOE_ERR_INVALID;
+  if (!aligned4(ids) || !aligned4(token_block) || !aligned4(sig) || (rejected && !aligned4(rejected)))
+    return MOE_ERR_UNSUPPORTED;
+  const int64_t blocks = (picks + eldr::kSigThreads - 1) / eldr::kSigThreads;
+  if (blocks > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
+  hipLaunchKernelGGL(eldr::sig_capture_kernel, dim3((unsigned)blocks), dim3(eldr::kSigThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream), ids, token_block, picks, T, K, layer0,
+                     L, E, num_blocks, reinterpret_cast<uint32_t*>(sig), rejected);
+  return launch_status();
+}
+
+extern "C" int moe_sig_reset(const int32_t* blocks, int32_t n, int32_t L, int32_t E,
+                             int32_t num_blocks, int8_t* sig, void* stream) {
+  using namespace eldr_host;
+  int st = check_sig_shape(L, E, num_blocks);
+  if (st != MOE_OK) return st;
+  if (n < 0) return MOE_ERR_INVALID;
+  if (n == 0 || num_blocks == 0) return MOE_OK;
+  if (n > 65535) return MOE_ERR_UNSUPPORTED;
+  if (!blocks || !sig) return MOE_ERR_INVALID;
+  if (!aligned4(blocks) || !aligned4(sig)) return MOE_ERR_UNSUPPORTED;
+  const int row_words = L * E / 4;
+  dim3 grid((row_words + eldr::kSigThreads - 1) / eldr::kSigThreads, n);
+  hipLaunchKernelGGL(eldr::sig_reset_kernel, grid, dim3(eldr::kSigThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream), blocks, row_words, num_blocks,
+                     reinterpret_cast<uint32_t*>(sig));
+  return launch_status();
+}
+
+extern "C" int moe_sig_request_counts(const int8_t* sig, const int32_t* block_table,
+                                      const int32_t* n_blocks, int32_t R, int32_t max_blocks,
+                                      int32_t L, int32_t E, int32_t num_blocks, int32_t* out,
+                                      void* stream) {
+  using namespace eldr_host;
+  int st = check_sig_shape(L, E, num_blocks);
+  if (st != MOE_OK) return st;
+  if (R < 0 || max_blocks < 0) return MOE_ERR_INVALID;
+  if (R == 0) return MOE_OK;
+  if (R > 65535) return MOE_ERR_UNSUPPORTED;
+  if (!n_blocks || !out || (max_blocks > 0 && !block_table) || (num_blocks > 0 && !sig))
+    return MOE_ERR_INVALID;
+  if (!aligned16(out) || !aligned4(n_blocks) || (block_table && !aligned4(block_table)) ||
+      (sig && !aligned4(sig)))
+    return MOE_ERR_UNSUPPORTED;
+  const int row_words = L * E / 4;
+  dim3 grid((row_words + eldr::kSigThreads - 1) / eldr::kSigThreads, R);
+  hipLaunchKernelGGL(eldr::sig_request_kernel, grid, dim3(eldr::kSigThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream),
+                     reinterpret_cast<const uint32_t*>(sig), block_table, n_blocks, max_blocks,
+                     row_words, num_blocks, reinterpret_cast<int4*>(out));
+  return launch_status();
+}

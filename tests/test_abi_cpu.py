@@ -19,7 +19,8 @@ def test_exports_every_declared_function(lib):
     names = B.header_functions()
     assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_expert_ffn_up",
             "moe_expert_ffn_down", "moe_combine", "moe_pack_weights",
-            "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version"} <= set(names)
+            "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version",
+            "moe_sig_capture", "moe_sig_reset", "moe_sig_request_counts"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -118,3 +119,27 @@ def test_pack_arguments_rejected(lib):
     assert lib.moe_pack_weights(FAKE, 2, 16, 32, FAKE, None) == B.MOE_ERR_INVALID       # in place
     assert lib.moe_pack_weights(FAKE_MIS, 2, 16, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED
     assert lib.moe_pack_weights(None, 0, 16, 32, None, None) == B.MOE_OK                # empty
+
+
+def test_signature_calls_validate_on_host(lib):
+    # moe_sig_capture(ids, token_block, n_layers, T, K, layer0, L, E, num_blocks, sig, rejected, stream)
+    cap = lib.moe_sig_capture
+    assert cap(FAKE, FAKE, 1, 64, 8, 0, 3, 7, 10, FAKE, None, None) == B.MOE_ERR_UNSUPPORTED  # L*E % 4
+    assert cap(FAKE, FAKE, 4, 64, 8, 45, 48, 128, 10, FAKE, None, None) == B.MOE_ERR_INVALID  # layers past L
+    assert cap(FAKE, FAKE, 1, 64, 9, 0, 4, 8, 10, FAKE, None, None) == B.MOE_ERR_INVALID      # K > E
+    assert cap(None, FAKE, 1, 64, 8, 0, 4, 128, 10, FAKE, None, None) == B.MOE_ERR_INVALID
+    assert cap(FAKE, FAKE, 1, 0, 8, 0, 4, 128, 10, None, None, None) == B.MOE_OK              # nothing to add
+    assert cap(FAKE, FAKE, 0, 64, 8, 0, 4, 128, 10, None, None, None) == B.MOE_OK
+    odd = ctypes.c_void_p(0x10002)
+    assert cap(FAKE, FAKE, 1, 64, 8, 0, 4, 128, 10, odd, None, None) == B.MOE_ERR_UNSUPPORTED
+    assert cap(FAKE, FAKE, 1, 64, 8, 0, 4, 512, 10, FAKE, None, None) == B.MOE_ERR_UNSUPPORTED  # E > 256
+    # moe_sig_reset(blocks, n, L, E, num_blocks, sig, stream)
+    assert lib.moe_sig_reset(FAKE, 0, 4, 128, 10, FAKE, None) == B.MOE_OK
+    assert lib.moe_sig_reset(FAKE, -1, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
+    assert lib.moe_sig_reset(None, 3, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
+    # moe_sig_request_counts(sig, table, n_blocks, R, max_blocks, L, E, num_blocks, out, stream)
+    rc = lib.moe_sig_request_counts
+    assert rc(FAKE, FAKE, FAKE, 0, 8, 4, 128, 10, FAKE, None) == B.MOE_OK
+    assert rc(FAKE, FAKE, FAKE, 3, 8, 4, 128, 10, FAKE_MIS, None) == B.MOE_ERR_UNSUPPORTED  # out needs 16 B
+    assert rc(FAKE, FAKE, None, 3, 8, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
+    assert rc(FAKE, FAKE, FAKE, -1, 8, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
