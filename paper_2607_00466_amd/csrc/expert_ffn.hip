@@ -435,9 +435,9 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
   } else {
     // Every wave builds the table of its XCD's experts in registers: lane m
     // holds expert m's id (union_ids is read together with union_size; it is
-    // -1 past the union), bucket start and size, its number of token groups,
-    // and the inclusive prefix sum of group counts.  An item is found with
-    // one ballot, and its expert's data with lane reads.
+    // -1 past the union), bucket start and size, and its number of token
+    // groups.  An item is found with one ballot, and its expert's data with
+    // lane reads.
     const int u_lane = xcd + kNumXcd * lane;
     int e_lane = -1;
     if (lane < kMaxExpertsPerXcd && u_lane < a.experts) e_lane = a.union_ids[u_lane];
@@ -454,18 +454,23 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
       c_lane = a.offsets[e_lane + 1] - sb_lane;
     }
     const int g_lane = member ? (c_lane + kGroupTokens - 1) / kGroupTokens : 0;
-    int incl = g_lane;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
+    // Items are ordered heaviest expert first (more tokens first, ties by
+    // union position), so the longest items start earliest: `before` is the
+    // number of token groups of the experts that precede this lane's.
+    int before = 0, total = 0;
+    for (int q = 0; q < M; ++q) {
+      const int cq = __builtin_amdgcn_readlane(c_lane, q);
+      const int gq = __builtin_amdgcn_readlane(g_lane, q);
+      if (cq > c_lane || (cq == c_lane && q < lane)) before += gq;
+      total += gq;
     }
-    const int items = __builtin_amdgcn_readlane(incl, kWave - 1) * a.tiles;
+    const int items = total * a.tiles;
     for (int item = slot; item < items; item += slots) {
-      // m = number of experts whose items all precede this one
-      const int m = __popcll(__ballot(incl * a.tiles <= item));
+      // the expert whose items cover this one
+      const int m = __ffsll((unsigned long long)__ballot(
+                        member && before * a.tiles <= item && item < (before + g_lane) * a.tiles)) - 1;
       const int g = __builtin_amdgcn_readlane(g_lane, m);
-      const int r = item - __builtin_amdgcn_readlane(incl - g_lane, m) * a.tiles;
+      const int r = item - __builtin_amdgcn_readlane(before, m) * a.tiles;
       const int tile = r / g;
       const int group = r - tile * g;
       const int p0 = group * kGroupTokens;
