@@ -176,12 +176,13 @@ class Bench:
 
 def calibration(reps: int = 10) -> dict:
     """What plain streaming achieves on this GPU, for context beside the 8 TB/s peak:
-    torch.sum over a 2 GiB fp32 tensor (reads) and a 2 GiB device-to-device copy
-    (reads + writes), best of `reps`, HIP events on the current stream."""
+    the library's streaming-read probe over 2 GiB (reads only) and a 2 GiB
+    device-to-device copy (reads + writes), best of `reps`, HIP events on the
+    current stream."""
     n = (2 << 30) // 4
     a = torch.ones(n, device="cuda")
     b = torch.empty_like(a)
-    s = torch.zeros((), device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
 
     def best(fn) -> float:
         fn()
@@ -197,13 +198,13 @@ def calibration(reps: int = 10) -> dict:
             t.append(e0.elapsed_time(e1))
         return min(t)
 
-    read_ms = best(lambda: torch.sum(a, dim=0, out=s))
+    read_ms = best(lambda: B.moe_stream_read_probe(a, sink))
     copy_ms = best(lambda: b.copy_(a))
     del a, b
     torch.cuda.empty_cache()
     return {"stream_read_GBps": round(4 * n / read_ms / 1e6, 1),
             "copy_GBps_read_plus_write": round(8 * n / copy_ms / 1e6, 1),
-            "how": "best of 10: torch.sum over a 2 GiB fp32 tensor; a 2 GiB device copy"}
+            "how": "best of 10: moe_stream_read_probe over 2 GiB; a 2 GiB device copy"}
 
 
 def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:

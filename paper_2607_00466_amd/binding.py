@@ -19,7 +19,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libeldr_moe.so")
 INCLUDE_DIR = os.path.join(os.path.dirname(_PKG), "include")
 HEADER_PATH = os.path.join(INCLUDE_DIR, "eldr_moe.h")
-HEADER_PATHS = (HEADER_PATH, os.path.join(INCLUDE_DIR, "eldr_signature.h"))
+HEADER_PATHS = (HEADER_PATH, os.path.join(INCLUDE_DIR, "eldr_signature.h"),
+                os.path.join(INCLUDE_DIR, "eldr_calibration.h"))
 
 MOE_OK = 0
 MOE_ERR_INVALID = -1
@@ -61,6 +62,7 @@ _SIGNATURES = {
     "moe_sig_capture": (ctypes.c_int, [_vp, _vp] + [ctypes.c_int32] * 7 + [_vp, _vp, _vp]),
     "moe_sig_reset": (ctypes.c_int, [_vp] + [ctypes.c_int32] * 4 + [_vp, _vp]),
     "moe_sig_request_counts": (ctypes.c_int, [_vp, _vp, _vp] + [ctypes.c_int32] * 5 + [_vp, _vp]),
+    "moe_stream_read_probe": (ctypes.c_int, [_vp, ctypes.c_size_t, _vp, _vp]),
 }
 
 _lib = None
@@ -331,3 +333,14 @@ def moe_sig_request_counts(sig, block_table, n_blocks, out=None, stream=None) ->
         _ptr(sig), _ptr(block_table), _ptr(n_blocks), R, max_blocks, L, E, nb, _ptr(out),
         _stream(stream)))
     return out
+
+
+# ----------------------------------------------------------------------------- calibration
+
+def moe_stream_read_probe(buf, sink, stream=None) -> None:
+    """Read all of buf once with the plain streaming kernel (measurement aid)."""
+    if buf.device.type != "cuda" or not buf.is_contiguous():
+        raise ValueError("buf: must be a contiguous device tensor")
+    _need(sink, "sink", torch.int32, 1)
+    _check("moe_stream_read_probe", load().moe_stream_read_probe(
+        _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))

@@ -20,7 +20,8 @@ def test_exports_every_declared_function(lib):
     assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_expert_ffn_up",
             "moe_expert_ffn_down", "moe_combine", "moe_pack_weights",
             "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version",
-            "moe_sig_capture", "moe_sig_reset", "moe_sig_request_counts"} <= set(names)
+            "moe_sig_capture", "moe_sig_reset", "moe_sig_request_counts",
+            "moe_stream_read_probe"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -143,3 +144,10 @@ def test_signature_calls_validate_on_host(lib):
     assert rc(FAKE, FAKE, FAKE, 3, 8, 4, 128, 10, FAKE_MIS, None) == B.MOE_ERR_UNSUPPORTED  # out needs 16 B
     assert rc(FAKE, FAKE, None, 3, 8, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
     assert rc(FAKE, FAKE, FAKE, -1, 8, 4, 128, 10, FAKE, None) == B.MOE_ERR_INVALID
+
+
+def test_stream_probe_validates_on_host(lib):
+    assert lib.moe_stream_read_probe(FAKE, 0, FAKE, None) == B.MOE_OK
+    assert lib.moe_stream_read_probe(None, 64, FAKE, None) == B.MOE_ERR_INVALID
+    assert lib.moe_stream_read_probe(FAKE, 24, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+    assert lib.moe_stream_read_probe(FAKE_MIS, 64, FAKE, None) == B.MOE_ERR_UNSUPPORTED

@@ -301,3 +301,15 @@ def test_pack_weights_is_the_documented_permutation(E, R, K):
     # fragment (e, band, step) holds, lane by lane, src[e, 16 band + l % 16, 32 step + 8 (l // 16) + j]
     ref = src.reshape(E, R // 16, 16, K // 32, 4, 8).transpose(0, 1, 3, 4, 2, 5).reshape(-1)
     assert np.array_equal(packed.reshape(-1), ref)
+
+
+def test_stream_probe_reads_without_writing():
+    # The calibration probe reads a buffer (a ragged size: not a multiple of its
+    # per-workgroup stretch) and leaves the sink alone unless its checksum hits
+    # the fixed constant, which all-ones data does not.
+    G.say("case: streaming-read probe over 3 MiB + 48 bytes")
+    buf = torch.ones((3 << 20) // 4 + 12, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.moe_stream_read_probe(buf, sink)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 0
