@@ -48,6 +48,7 @@ _STREAM_GATE = 1
 _STREAM_EXPERTS = 2
 _STREAM_ROUTING = 3
 _STREAM_PREFILL = 4
+_STREAM_REQUESTS = 5
 _N_STREAMS = 8
 
 
@@ -233,4 +234,40 @@ def prefill_picks(n_layers: int, T: int, E: int, K: int, seed: int = 0, skew: fl
                 out[layer, t] = order[rng.choice(E, size=K, replace=False, p=p)]
             else:
                 out[layer, t] = rng.choice(E, size=K, replace=False)
+    return out
+
+
+def domain_pick_probs(model: DomainModel, subsets: np.ndarray, domain: int, layer: int) -> np.ndarray:
+    """Per-expert pick propensities of one domain at one layer, float64 [E]:
+    p_domain times the truncated Zipf(s) weight of the expert's rank in the
+    domain's subset, plus (1 - p_domain) / E for every expert."""
+    ranks = np.arange(1, model.subset_size + 1, dtype=np.float64)
+    pz = ranks ** (-model.zipf_s)
+    pz /= pz.sum()
+    p = np.full(model.E, (1.0 - model.p_domain) / model.E)
+    p[subsets[domain, layer]] += model.p_domain * pz
+    return p
+
+
+def domain_requests(model: DomainModel, subsets: np.ndarray, domains: np.ndarray, n_tokens: int,
+                    seed: int = 0, stream: int = 0) -> np.ndarray:
+    """Top-k picks of n_tokens tokens of each request, at every layer:
+    int32 [n_layers, n_requests, n_tokens, K].
+
+    A token of a request with domain d takes its K distinct picks at layer l
+    by successive draws from domain_pick_probs(d, l), each draw excluding the
+    experts already picked (Gumbel-top-K over log-propensities, which is that
+    successive sampling).  Vectorised; `stream` separates independent draws
+    (for example a request's prefill and its decode steps).
+    """
+    n_layers = subsets.shape[1]
+    R = len(domains)
+    rng = _rng(seed, _STREAM_REQUESTS, stream, R, n_tokens, n_layers)
+    out = np.empty((n_layers, R, n_tokens, model.K), dtype=np.int32)
+    for layer in range(n_layers):
+        logp = np.log(np.stack([domain_pick_probs(model, subsets, d, layer)
+                                for d in range(model.n_domains)]))
+        keys = logp[domains][:, None, :] + rng.gumbel(size=(R, n_tokens, model.E))
+        top = np.argpartition(-keys, model.K - 1, axis=2)[:, :, :model.K]
+        out[layer] = top.astype(np.int32)
     return out
