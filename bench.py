@@ -476,6 +476,137 @@ def signature_workload(path: str, reps: int = 20) -> None:
             log(f"signature {rec['call']}: {rec['us']} us")
 
 
+def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_timed: int = 8) -> None:
+    """ELDR end to end on synthetic domain traffic (Design: Expert Signature,
+    Offline clustering, Online routing), against round-robin.
+
+    1024 calibration requests (8 domains, 48 MoE layers, E=128, top-8) give
+    prefill counts and decode activation probabilities; the native library
+    fits the IDF table, the greedy layer mask and a Hungarian-balanced
+    K-means with one centroid per worker.  Then workers * per_worker new
+    requests are routed by locality-band routing (tau = 0.1) and by
+    round-robin; each worker's decode step (one token per request) is drawn
+    from its requests' domains, and its union per layer is counted.  Finally
+    each worker's step is run on the GPU for `layers_timed` layers through
+    the MoE layer (Qwen3-30B-A3B-shaped weights, controlled routing = the
+    drawn picks) and timed."""
+    model = synth.DomainModel()
+    L, E, K, N_cal, pre_tok, dec_tok = 48, model.E, model.K, 1024, 32, 16
+    subsets = synth.domain_subsets(model, L, seed=0)
+
+    def counts_of(ids):  # ids [L, R, T, K] -> counts [R, L, E]
+        R = ids.shape[1]
+        out = np.zeros((R, L, E), np.int32)
+        for layer in range(L):
+            for r in range(R):
+                out[r, layer] = np.bincount(ids[layer, r].ravel(), minlength=E)
+        return out
+
+    rng = np.random.default_rng(7)
+    cal_dom = rng.integers(0, model.n_domains, N_cal)
+    cal_counts = counts_of(synth.domain_requests(model, subsets, cal_dom, pre_tok, seed=1, stream=0))
+    P = counts_of(synth.domain_requests(model, subsets, cal_dom, dec_tok, seed=1, stream=1)).reshape(N_cal, -1)
+    P = (P / np.linalg.norm(P, axis=1, keepdims=True)).astype(np.float32)
+    pairs = rng.choice(N_cal, (4000, 2))
+    pairs = pairs[pairs[:, 0] != pairs[:, 1]]
+    t0 = time.perf_counter()
+    idf = B.eldr_idf(cal_counts)
+    order, curve, n_star = B.eldr_greedy_layers(cal_counts, idf, P, pairs)
+    mask = order[:n_star].tolist()
+    S_cal = np.stack([B.eldr_signature(c, idf, mask) for c in cal_counts])
+    init = rng.choice(N_cal, workers, replace=False)
+    C, _, iters = B.eldr_balanced_kmeans(S_cal, workers, init, max_iters=50)
+    fit_s = time.perf_counter() - t0
+    log(f"routing: offline fit {fit_s:.2f} s (N*={n_star} of {L} layers, rho {curve[n_star - 1]:.3f}, "
+        f"k-means {iters} iterations)")
+
+    R = workers * per_worker
+    dom = rng.integers(0, model.n_domains, R)
+    req_counts = counts_of(synth.domain_requests(model, subsets, dom, pre_tok, seed=2, stream=0))
+    S = np.stack([B.eldr_signature(c, idf, mask) for c in req_counts])
+    t0 = time.perf_counter()
+    eldr_w, eldr_loads = B.eldr_route_batch(S, C, np.zeros(workers, np.int32), 0.1)
+    route_us = (time.perf_counter() - t0) / R * 1e6
+    rr_w = np.arange(R) % workers
+    step = synth.domain_requests(model, subsets, dom, 1, seed=2, stream=2)[:, :, 0, :]  # [L, R, K]
+
+    shape = synth.SHAPES["qwen3_30b_a3b"]
+    raw = synth.expert_weights(shape, 0, 0, device="cuda")
+    packed = [B.pack_expert_weights(*raw)]
+    packed.append(tuple(w.clone() for w in packed[0]))
+    del raw
+    wg = torch.from_numpy(synth.gate_weights(shape, 0, 0)).cuda()
+    results = {}
+    for name, assign in (("eldr", eldr_w), ("round_robin", rr_w)):
+        unions = np.zeros((workers, L))
+        sizes = np.bincount(assign, minlength=workers)
+        for w in range(workers):
+            members = np.nonzero(assign == w)[0]
+            for layer in range(L):
+                unions[w, layer] = len(np.unique(step[layer, members]))
+        # GPU: each worker's step over the first layers_timed layers
+        worker_us = []
+        for w in range(workers):
+            members = np.nonzero(assign == w)[0]
+            T = len(members)
+            if T == 0:
+                worker_us.append(0.0)
+                continue
+            d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+            buf = B.LayerBuffers.allocate(d)
+            x = torch.from_numpy(synth.hidden_states(T, shape.H, 0, w)).cuda()
+            routes = []
+            for layer in range(layers_timed):
+                ids = torch.from_numpy(np.ascontiguousarray(step[layer, members])).cuda()
+                wts = torch.from_numpy(synth.dirichlet_weights(T, K, np.random.default_rng(layer))).cuda()
+                routes.append((ids, wts))
+
+            def run():
+                for layer in range(layers_timed):
+                    w1, w3, w2 = packed[layer % 2]
+                    B.moe_layer(x, wg, w1, w3, w2, d, buf, routing=routes[layer])
+
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                run()
+            torch.cuda.current_stream().wait_stream(side)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run()
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(10):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            worker_us.append(e0.elapsed_time(e1) / 10 * 1e3)
+            del g, buf
+        results[name] = {"mean_union": float(unions.mean()), "max_batch": int(sizes.max()),
+                         "min_batch": int(sizes.min()),
+                         "mean_worker_step_us": float(np.mean(worker_us)),
+                         "max_worker_step_us": float(np.max(worker_us))}
+    e, r = results["eldr"], results["round_robin"]
+    rec = {"workload": f"ELDR vs round-robin: {workers} workers x {per_worker} requests, 8 synthetic domains, "
+                       f"48 MoE layers (E=128, top-8); decode step timed on {layers_timed} Qwen3-30B-A3B-shaped layers",
+           "fit_s": round(fit_s, 2), "n_star": n_star, "rho": round(float(curve[n_star - 1]), 4),
+           "kmeans_iterations": iters, "route_us_per_request": round(route_us, 2),
+           "eldr": e, "round_robin": r,
+           "union_reduction": round(1 - e["mean_union"] / r["mean_union"], 4),
+           "mean_step_reduction": round(1 - e["mean_worker_step_us"] / r["mean_worker_step_us"], 4),
+           "max_step_reduction": round(1 - e["max_worker_step_us"] / r["max_worker_step_us"], 4)}
+    with open(path, "a") as f:
+        f.write(json.dumps(rec) + "\n")
+    log(f"routing: union per worker-layer {e['mean_union']:.1f} (ELDR) vs {r['mean_union']:.1f} (RR): "
+        f"{100 * rec['union_reduction']:.1f}% fewer; worker decode step {e['mean_worker_step_us']:.0f} vs "
+        f"{r['mean_worker_step_us']:.0f} us ({100 * rec['mean_step_reduction']:.1f}% less); batch sizes "
+        f"{e['min_batch']}-{e['max_batch']} (ELDR)")
+    del packed
+    torch.cuda.empty_cache()
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -488,6 +619,9 @@ def main() -> int:
                     help="also time the expert-signature cache calls, appending JSON lines to this file")
     ap.add_argument("--signature-only", action="store_true",
                     help="run only the --signature measurement (no layer bench line)")
+    ap.add_argument("--routing", default="",
+                    help="also run ELDR routing vs round-robin end to end (native fit + routing, GPU "
+                         "decode steps), appending a JSON line to this file")
     ap.add_argument("--multilayer", default="",
                     help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
                          "appending JSON lines to this file")
@@ -502,6 +636,8 @@ def main() -> int:
     B.load()
     if args.signature_only:
         signature_workload(args.signature or "signature.jsonl")
+        if args.routing:
+            routing_workload(args.routing)
         return 0
     shape = synth.SHAPES["qwen3_30b_a3b"]
     T = 64
@@ -551,6 +687,8 @@ def main() -> int:
         sweep(args.sweep, max(20, args.steps // 2), args.warmup)
     if args.signature:
         signature_workload(args.signature)
+    if args.routing:
+        routing_workload(args.routing)
     if args.multilayer:
         domain_workload(args.multilayer, 10, 2)
         gpt_oss_workload(args.multilayer, 5, 1)

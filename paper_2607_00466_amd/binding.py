@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_PKG, "libeldr_moe.so")
 INCLUDE_DIR = os.path.join(os.path.dirname(_PKG), "include")
 HEADER_PATH = os.path.join(INCLUDE_DIR, "eldr_moe.h")
 HEADER_PATHS = (HEADER_PATH, os.path.join(INCLUDE_DIR, "eldr_signature.h"),
-                os.path.join(INCLUDE_DIR, "eldr_calibration.h"))
+                os.path.join(INCLUDE_DIR, "eldr_calibration.h"),
+                os.path.join(INCLUDE_DIR, "eldr_route.h"))
 
 MOE_OK = 0
 MOE_ERR_INVALID = -1
@@ -63,6 +64,19 @@ _SIGNATURES = {
     "moe_sig_reset": (ctypes.c_int, [_vp] + [ctypes.c_int32] * 4 + [_vp, _vp]),
     "moe_sig_request_counts": (ctypes.c_int, [_vp, _vp, _vp] + [ctypes.c_int32] * 5 + [_vp, _vp]),
     "moe_stream_read_probe": (ctypes.c_int, [_vp, ctypes.c_size_t, _vp, _vp]),
+    "eldr_idf": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp]),
+    "eldr_signature": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
+                                      ctypes.c_int32, _vp]),
+    "eldr_rho": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int32, _vp,
+                                ctypes.c_int32, _vp]),
+    "eldr_greedy_layers": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
+                                          _vp, ctypes.c_int32, _vp, ctypes.c_int32, _vp, _vp, _vp]),
+    "eldr_balanced_kmeans": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                            _vp, ctypes.c_int32, _vp, _vp, _vp]),
+    "eldr_route": (ctypes.c_int, [_vp, ctypes.c_int32, _vp, ctypes.c_int32, _vp, ctypes.c_float,
+                                  _vp]),
+    "eldr_route_batch": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int32,
+                                        _vp, ctypes.c_float, _vp]),
 }
 
 _lib = None
@@ -87,7 +101,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
 def header_functions(paths=HEADER_PATHS) -> list[str]:
     """Names of the functions the headers under include/ declare."""
     text = "\n".join(open(p).read() for p in paths)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(moe_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?((?:moe|eldr)_\w+)\s*\(", text,
+                                 re.M)))
 
 
 def status_string(status: int) -> str:
@@ -344,3 +359,110 @@ def moe_stream_read_probe(buf, sink, stream=None) -> None:
     _need(sink, "sink", torch.int32, 1)
     _check("moe_stream_read_probe", load().moe_stream_read_probe(
         _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- routing (host)
+
+def _host(a, dtype):
+    """A C-contiguous NumPy array of `dtype` and a pointer to it (host memory)."""
+    import numpy as np
+
+    arr = np.ascontiguousarray(a, dtype=dtype)
+    return arr, ctypes.c_void_p(arr.ctypes.data)
+
+
+def eldr_idf(counts):
+    """IDF table [L, E] float32 from calibration counts [N, L, E]."""
+    import numpy as np
+
+    c, pc = _host(counts, np.int32)
+    N, L, E = c.shape
+    out = np.empty((L, E), np.float32)
+    _check("eldr_idf", load().eldr_idf(pc, N, L, E, ctypes.c_void_p(out.ctypes.data)))
+    return out
+
+
+def eldr_signature(counts, idf, layers):
+    """Signature [len(layers) * E] float32 of one request's counts [L, E]."""
+    import numpy as np
+
+    c, pc = _host(counts, np.int32)
+    w, pw = _host(idf, np.float32)
+    ly, pl = _host(layers, np.int32)
+    L, E = c.shape
+    out = np.empty(len(ly) * E, np.float32)
+    _check("eldr_signature", load().eldr_signature(pc, pw, L, E, pl, len(ly),
+                                                   ctypes.c_void_p(out.ctypes.data)))
+    return out
+
+
+def eldr_rho(S, P, pairs) -> float:
+    import numpy as np
+
+    s, ps = _host(S, np.float32)
+    p, pp = _host(P, np.float32)
+    pr, ppr = _host(pairs, np.int32)
+    out = ctypes.c_double(0.0)
+    _check("eldr_rho", load().eldr_rho(ps, s.shape[0], s.shape[1], pp, p.shape[1], ppr, pr.shape[0],
+                                       ctypes.byref(out)))
+    return out.value
+
+
+def eldr_greedy_layers(counts, idf, P, pairs):
+    """(order [L], rho curve [L], N*) of greedy layer selection."""
+    import numpy as np
+
+    c, pc = _host(counts, np.int32)
+    w, pw = _host(idf, np.float32)
+    p, pp = _host(P, np.float32)
+    pr, ppr = _host(pairs, np.int32)
+    N, L, E = c.shape
+    order = np.empty(L, np.int32)
+    curve = np.empty(L, np.float64)
+    n_star = ctypes.c_int32(0)
+    _check("eldr_greedy_layers", load().eldr_greedy_layers(
+        pc, N, L, E, pw, pp, p.shape[1], ppr, pr.shape[0], ctypes.c_void_p(order.ctypes.data),
+        ctypes.c_void_p(curve.ctypes.data), ctypes.byref(n_star)))
+    return order, curve, n_star.value
+
+
+def eldr_balanced_kmeans(S, K: int, init, max_iters: int = 50):
+    """(centroids [K, d] float32, assignment [N] int32, iterations) of balanced K-means."""
+    import numpy as np
+
+    s, ps = _host(S, np.float32)
+    ini, pi = _host(init, np.int32)
+    N, d = s.shape
+    C = np.empty((K, d), np.float32)
+    assign = np.empty(N, np.int32)
+    iters = ctypes.c_int32(0)
+    _check("eldr_balanced_kmeans", load().eldr_balanced_kmeans(
+        ps, N, d, K, pi, max_iters, ctypes.c_void_p(C.ctypes.data),
+        ctypes.c_void_p(assign.ctypes.data), ctypes.byref(iters)))
+    return C, assign, iters.value
+
+
+def eldr_route(s, centroids, loads, tau: float) -> int:
+    import numpy as np
+
+    v, pv = _host(s, np.float32)
+    c, pc = _host(centroids, np.float32)
+    ld, pld = _host(loads, np.int32)
+    out = ctypes.c_int32(-1)
+    _check("eldr_route", load().eldr_route(pv, v.shape[0], pc, c.shape[0], pld, tau,
+                                           ctypes.byref(out)))
+    return out.value
+
+
+def eldr_route_batch(S, centroids, loads, tau: float):
+    """Route the rows of S in order; returns (workers [R], loads after routing [K])."""
+    import numpy as np
+
+    s, ps = _host(S, np.float32)
+    c, pc = _host(centroids, np.float32)
+    ld = np.array(loads, dtype=np.int32, copy=True)
+    workers = np.empty(s.shape[0], np.int32)
+    _check("eldr_route_batch", load().eldr_route_batch(
+        ps, s.shape[0], s.shape[1], pc, c.shape[0], ctypes.c_void_p(ld.ctypes.data), tau,
+        ctypes.c_void_p(workers.ctypes.data)))
+    return workers, ld

@@ -1,4 +1,5 @@
-"""Build libeldr_moe.so (gfx950) in-tree from csrc/*.hip with hipcc.
+"""Build libeldr_moe.so (gfx950) in-tree: csrc/*.hip with hipcc, and the
+host-only csrc/*.cpp (the routing library) with the host C++ compiler.
 
     python -m paper_2607_00466_amd.build
 
@@ -22,6 +23,8 @@ LIB = os.path.join(PKG, "libeldr_moe.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CXX = os.environ.get("CXX_HOST", "g++")
+CXXFLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
     "-Wno-unused-result",
@@ -45,8 +48,10 @@ def _run(cmd: list[str]) -> None:
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    objs = [os.path.join(BUILD, os.path.basename(s) + ".o") for s in srcs]
+    host = sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+    objs = [os.path.join(BUILD, os.path.basename(s) + ".o") for s in srcs + host]
     jobs = [[HIPCC, *FLAGS, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+    jobs += [[CXX, *CXXFLAGS, "-c", s, "-o", o] for s, o in zip(host, objs[len(srcs):])]
     with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         for f in [ex.submit(_run, j) for j in jobs]:
             f.result()

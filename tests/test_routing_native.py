@@ -1,0 +1,124 @@
+"""The native routing library (include/eldr_route.h) against the routing oracle.
+
+Host code, so these run without a GPU.  Inputs are synthetic calibration
+requests from the domain generator (prefill counts, decode-time activation
+probabilities).  Integer decisions (layer order, N*, cluster assignment,
+routed worker) must match exactly; real values within float32 rounding.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import routing as RO
+from paper_2607_00466_amd import binding as B
+from paper_2607_00466_amd import synth
+
+
+@pytest.fixture(scope="module")
+def calib():
+    """64 calibration requests over 8 domains, 6 layers, E=32, top-4."""
+    model = synth.DomainModel(E=32, K=4, n_domains=8, subset_size=8)
+    L, N = 6, 64
+    subsets = synth.domain_subsets(model, L, seed=1)
+    domains = np.arange(N) % model.n_domains
+    pre = synth.domain_requests(model, subsets, domains, 24, seed=2, stream=0)   # [L, N, 24, K]
+    dec = synth.domain_requests(model, subsets, domains, 16, seed=2, stream=1)   # decode steps
+    counts = np.zeros((N, L, model.E), np.int32)
+    P = np.zeros((N, L, model.E))
+    for l in range(L):
+        for r in range(N):
+            counts[r, l] = np.bincount(pre[l, r].ravel(), minlength=model.E)
+            P[r, l] = np.bincount(dec[l, r].ravel(), minlength=model.E) / 16.0
+    P = P.reshape(N, -1)
+    P /= np.linalg.norm(P, axis=1, keepdims=True)
+    pairs = np.array(list(itertools.combinations(range(N), 2)))[::7]
+    return dict(counts=counts, P=P.astype(np.float32), pairs=pairs, domains=domains, L=L, E=model.E)
+
+
+def test_idf_matches(calib):
+    got = B.eldr_idf(calib["counts"])
+    ref = RO.idf_table(calib["counts"])
+    assert np.allclose(got, ref, rtol=1e-6, atol=0)
+
+
+def test_signature_matches(calib):
+    idf = B.eldr_idf(calib["counts"])
+    for r in (0, 5, 17):
+        for layers in ([0, 1, 2, 3, 4, 5], [4, 1], [3]):
+            got = B.eldr_signature(calib["counts"][r], idf, layers)
+            ref = RO.signature(calib["counts"][r], idf.astype(np.float64), layers)
+            assert np.allclose(got, ref, rtol=0, atol=2e-7)
+    assert not B.eldr_signature(np.zeros((2, 4), np.int32), np.ones((2, 4), np.float32), [0, 1]).any()
+
+
+def test_rho_matches(calib):
+    idf = B.eldr_idf(calib["counts"])
+    S = np.stack([B.eldr_signature(c, idf, list(range(calib["L"]))) for c in calib["counts"]])
+    got = B.eldr_rho(S, calib["P"], calib["pairs"])
+    ref = RO.rho(S.astype(np.float64), calib["P"].astype(np.float64), calib["pairs"])
+    assert abs(got - ref) < 1e-9
+
+
+def test_greedy_layers_match(calib):
+    idf = B.eldr_idf(calib["counts"])
+    order, curve, n_star = B.eldr_greedy_layers(calib["counts"], idf, calib["P"], calib["pairs"])
+    r_order, r_curve, r_star = RO.greedy_layers(calib["counts"], idf.astype(np.float64),
+                                                calib["P"].astype(np.float64), calib["pairs"])
+    assert order.tolist() == r_order
+    assert np.allclose(curve, r_curve, atol=1e-9)
+    assert n_star == r_star
+
+
+def test_balanced_kmeans_matches(calib):
+    idf = B.eldr_idf(calib["counts"])
+    S = np.stack([B.eldr_signature(c, idf, list(range(calib["L"]))) for c in calib["counts"]])
+    init = np.random.default_rng(3).choice(len(S), 8, replace=False)
+    C, assign, iters = B.eldr_balanced_kmeans(S, 8, init, max_iters=30)
+    rC, rassign, riters = RO.balanced_kmeans(S.astype(np.float64), 8, init, max_iters=30)
+    assert assign.tolist() == rassign.tolist()
+    assert iters == riters
+    assert np.allclose(C, rC, atol=2e-6)
+    assert np.bincount(assign, minlength=8).max() <= 8  # ceil(64 / 8)
+    # the domains are recovered: each cluster is one domain
+    for k in range(8):
+        assert len(set(calib["domains"][assign == k])) == 1
+
+
+def test_balanced_kmeans_capacity_ragged():
+    rng = np.random.default_rng(4)
+    S = rng.random((53, 10)).astype(np.float32)
+    S[:40, 0] += 5  # a dense region holding most points
+    S /= np.linalg.norm(S, axis=1, keepdims=True)
+    init = rng.choice(53, 6, replace=False)
+    C, assign, _ = B.eldr_balanced_kmeans(S, 6, init)
+    rC, rassign, _ = RO.balanced_kmeans(S.astype(np.float64), 6, init)
+    assert assign.tolist() == rassign.tolist()
+    assert np.bincount(assign, minlength=6).max() <= 9  # ceil(53 / 6)
+
+
+def test_route_matches(calib):
+    rng = np.random.default_rng(5)
+    idf = B.eldr_idf(calib["counts"])
+    S = np.stack([B.eldr_signature(c, idf, list(range(calib["L"]))) for c in calib["counts"]])
+    C = S[rng.choice(len(S), 5, replace=False)]
+    for tau in (0.0, 0.05, 0.1, 0.3, 1.0):
+        loads = rng.integers(0, 6, 5)
+        for r in range(len(S)):
+            assert B.eldr_route(S[r], C, loads, tau) == RO.route(S[r].astype(np.float64),
+                                                                 C.astype(np.float64), loads, tau)
+    workers, final = B.eldr_route_batch(S, C, np.zeros(5, np.int32), 0.1)
+    loads = np.zeros(5, np.int64)
+    for r in range(len(S)):
+        w = RO.route(S[r].astype(np.float64), C.astype(np.float64), loads, 0.1)
+        assert workers[r] == w
+        loads[w] += 1
+    assert final.tolist() == loads.tolist()
+
+
+def test_invalid_arguments_rejected():
+    lib = B.load()
+    assert lib.eldr_idf(None, 1, 1, 1, None) == B.MOE_ERR_INVALID
+    assert lib.eldr_balanced_kmeans(None, 4, 2, 8, None, 10, None, None, None) == B.MOE_ERR_INVALID
+    with pytest.raises(B.MoeError):
+        B.eldr_signature(np.zeros((2, 4), np.int32), np.ones((2, 4), np.float32), [0, 2])  # layer 2 >= L
