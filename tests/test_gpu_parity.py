@@ -290,6 +290,54 @@ def test_graph_replay_matches_eager():
     assert not torch.equal(eager, eager2)
 
 
+def test_graph_replay_large_batch_token_groups():
+    # A domain-clustered batch of 128 tokens (the >64-token mapping: token
+    # groups, heaviest experts first) captured in a graph: every replay equals
+    # the eager result bit for bit, and the output matches the oracle.
+    G.say("case: qwen layer T=128 domain-clustered (token groups), graph replays vs eager vs oracle")
+    model = synth.DomainModel()
+    subsets = synth.domain_subsets(model, 1, seed=0)
+    doms = synth.domain_batches(model, 128)["same_3"]
+    ids, w = synth.domain_routing(model, subsets, doms, 0, seed=0)
+    layer = G.Layer(QWEN, 128, seed=9)
+    g0 = layer.run(routing=(ids, w))
+    assert g0["counts"].max() > 64  # some expert really has more than one token group
+    _full_check(layer, g0, False, routing=(ids.astype(np.int64), w))
+    d, buf = layer.d, layer.buf
+    r = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p1, layer.p3, layer.p2, d, buf, routing=r)  # noqa: E731
+    eager = buf.out.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        buf.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf.out, eager), f"replay {rep}"
+        scratch = torch.randn(2048, device="cuda").sum()  # unrelated eager work between replays
+        torch.cuda.synchronize()
+        del scratch
+
+
+def test_batch_of_65_tokens_crosses_the_group_boundary():
+    # 65 tokens all on the same 8 experts: one group of 64 and one of 1.
+    G.say("case: qwen layer, T=65, all tokens on experts 3..10 (two token groups each)")
+    layer = G.Layer(QWEN, 65, seed=10)
+    ids = np.tile(np.arange(3, 11, dtype=np.int32), (65, 1))
+    w = np.random.default_rng(11).dirichlet(np.ones(8), size=65).astype(np.float32)
+    g = layer.run(routing=(ids, w))
+    assert g["counts"][3:11].tolist() == [65] * 8
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
 @pytest.mark.parametrize("E,R,K", [(3, 16, 32), (2, 48, 96), (128, 768, 2048), (5, 2880, 2880)])
 def test_pack_weights_is_the_documented_permutation(E, R, K):
     G.say(f"case: pack E={E} R={R} K={K}")
