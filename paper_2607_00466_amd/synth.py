@@ -31,6 +31,12 @@ Routing generators (used when the gate is bypassed) return ``ids`` [T, K]
 int32 (distinct within a token) and ``weights`` [T, K] fp32 summing to one per
 token.  ``prefill_picks`` draws the picks of a prefill forward over many MoE
 layers, for the expert-signature cache.
+
+``mxfp4_expert_weights`` gives the same draws quantized to MXFP4 (the format
+the paper serves GPT-OSS-120B in, Evaluation "Models"), per the OCP
+Microscaling specification: FP4 E2M1 codes, two a byte with the lower index in
+the low nibble, [E, R, K/2] uint8, and one E8M0 scale per 32 values along the
+reduction axis, [E, R, K/32] uint8.
 """
 from __future__ import annotations
 
@@ -124,6 +130,61 @@ def expert_weights(shape: LayerShape, seed: int = 0, layer: int = 0, device: str
             w[e].copy_(tmp.mul_(WEIGHT_STD))
         out.append(w)
     return out[0], out[1], out[2]
+
+
+def _mxfp4_quantize(w: torch.Tensor) -> tuple[torch.Tensor, torch.Tensor]:
+    """fp32 [R, K] -> MXFP4 (codes uint8 [R, K/2], scales uint8 [R, K/32]).
+
+    The conversion of the OCP Microscaling specification: per block of 32
+    consecutive values, shared exponent floor(log2(max |v|)) - 2 (2 is the
+    largest exponent of FP4 E2M1), stored as the E8M0 code exponent + 127;
+    each v / 2^exponent is rounded to the nearest E2M1 magnitude
+    {0, 0.5, 1, 1.5, 2, 3, 4, 6} (ties to the even code), saturating at 6.
+    Two codes a byte, the lower index in the low nibble.  This only makes
+    inputs: the layer's arithmetic (dequantization included) is elsewhere.
+    """
+    R, K = w.shape
+    v = w.reshape(R, K // 32, 32)
+    amax = v.abs().amax(dim=-1)
+    _, ex = torch.frexp(amax)                       # amax = m * 2^ex, m in [0.5, 1)
+    shared = (ex - 1 - 2).clamp(-126, 125)          # codes 1 .. 252
+    scaled = torch.ldexp(v, (-shared).unsqueeze(-1).to(v.dtype))
+    mag = scaled.abs()
+    # index into the E2M1 magnitudes; at a midpoint '>' keeps the lower (even)
+    # code and '>=' takes the upper (even) one
+    idx = ((mag > 0.25).to(torch.uint8) + (mag >= 0.75) + (mag > 1.25) + (mag >= 1.75)
+           + (mag > 2.5) + (mag >= 3.5) + (mag > 5.0))
+    sign = ((scaled < 0) & (idx > 0)).to(torch.uint8) << 3
+    nib = (idx | sign).reshape(R, K)
+    codes = nib[:, 0::2] | (nib[:, 1::2] << 4)
+    scales = (shared + 127).to(torch.uint8)
+    return codes.contiguous(), scales.contiguous()
+
+
+def mxfp4_expert_weights(shape: LayerShape, seed: int = 0, layer: int = 0, device: str = "cpu",
+                         experts: int | None = None) -> dict[str, tuple[torch.Tensor, torch.Tensor]]:
+    """MXFP4 expert weights {"w1", "w3", "w2": (codes, scales)} as torch uint8.
+
+    The fp32 N(0, 0.02) draws are those of ``expert_weights`` (same generator,
+    seed and order), quantized per OCP MX instead of rounded to bf16: codes
+    [E, R, K/2] and scales [E, R, K/32], blocks along the reduction axis.
+    """
+    E = shape.E if experts is None else experts
+    dev = torch.device(device)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(_torch_seed(seed, _STREAM_EXPERTS, layer))
+    out = {}
+    for name, (rows, cols) in (("w1", (shape.I, shape.H)), ("w3", (shape.I, shape.H)),
+                               ("w2", (shape.H, shape.I))):
+        codes = torch.empty((E, rows, cols // 2), dtype=torch.uint8, device=dev)
+        scales = torch.empty((E, rows, cols // 32), dtype=torch.uint8, device=dev)
+        for e in range(E):
+            tmp = torch.randn((rows, cols), generator=gen, dtype=torch.float32, device=dev)
+            c, s = _mxfp4_quantize(tmp.mul_(WEIGHT_STD))
+            codes[e].copy_(c)
+            scales[e].copy_(s)
+        out[name] = (codes, scales)
+    return out
 
 
 def bf16_bits(t: torch.Tensor) -> np.ndarray:

@@ -81,3 +81,20 @@ def test_domain_routing():
                     for d in range(8)])
     mixed = len(set(synth.domain_routing(m, subs, batches["mixed"], 0)[0].ravel().tolist()))
     assert same < mixed
+
+
+def test_mxfp4_weights_shapes_and_determinism():
+    sh = synth.SHAPES["tiny"]
+    a = synth.mxfp4_expert_weights(sh, seed=3, experts=2)
+    b = synth.mxfp4_expert_weights(sh, seed=3, experts=2)
+    for name, (rows, cols) in (("w1", (sh.I, sh.H)), ("w3", (sh.I, sh.H)), ("w2", (sh.H, sh.I))):
+        c, s = a[name]
+        assert c.dtype == torch.uint8 and s.dtype == torch.uint8
+        assert tuple(c.shape) == (2, rows, cols // 2) and tuple(s.shape) == (2, rows, cols // 32)
+        assert torch.equal(c, b[name][0]) and torch.equal(s, b[name][1])
+        assert 1 <= int(s.min()) and int(s.max()) <= 252
+    # the same fp32 draws as the bf16 weights: both round the same numbers
+    w1 = synth.expert_weights(sh, seed=3, experts=2)[0].float()
+    c, s = a["w1"]
+    X = torch.pow(2.0, s.float() - 127).repeat_interleave(32, dim=-1)
+    assert (w1.abs() <= 8 * X).all()
