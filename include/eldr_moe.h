@@ -190,6 +190,71 @@ int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offse
                         void* stream);
 
 /*
+ * MXFP4 expert weights (Evaluation, "Models": GPT-OSS-120B is served in
+ * mxfp4).  The format is the OCP Microscaling (MX) v1.0 MXFP4: blocks of 32
+ * values along the reduction axis share one E8M0 scale X = 2^(code - 127);
+ * each value is an FP4 E2M1 code (sign, 2-bit exponent with bias 1, 1-bit
+ * mantissa: magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6) and stands for X times
+ * its magnitude.  Unpacked tensors, as checkpoints store them:
+ *   codes  [E, R, K/2] uint8, value k of a row in byte k/2, the even k in
+ *          the low nibble;
+ *   scales [E, R, K/32] uint8, the scale of values 32 j .. 32 j + 31 at j.
+ * Scale codes must lie in 1 .. 252 (every dequantized value is then a finite
+ * bf16 number); 0, 253 .. 255 are not supported and are not checked.
+ *
+ * moe_pack_mxfp4_up / moe_pack_mxfp4_down -- permute the unpacked W1 and W3
+ * ([E, I, H]) or W2 ([E, H, I]) into the layout the MXFP4 FFN streams, once,
+ * off the decode path.  For each expert, band (up: 16 rows of W1 and the same
+ * 16 rows of W3; down: 32 rows of W2), slot s of two k-steps (64 values:
+ * H/64 slots up, I/64 down) and lane l (0 .. 63), 16 bytes: the 4 code bytes
+ * of row l % 16 and values 64 s + 8 (l / 16) .. + 7, then the same for
+ * 64 s + 32 + 8 (l / 16), of tile 0 (up: W1; down: the band's first 16
+ * rows), then both again for tile 1 (up: W3; down: the band's last 16 rows).
+ * Scales: for each expert, band and slot, 16 dwords (row 0 .. 15), each the
+ * 4 scale bytes in that same order.  codes receives E*I*H bytes (up) or
+ * E*H*I/2 (down), scales E*I*H/16 (up) or E*H*I/32 (down): the unpacked
+ * sizes.  Inputs and outputs are distinct device buffers; code inputs and
+ * scale outputs 4-byte aligned, code outputs 16-byte aligned.  Requires
+ * H % 64 == 0 and I % 64 == 0.  Asynchronous on `stream`.
+ */
+int moe_pack_mxfp4_up(const uint8_t* w1_codes, const uint8_t* w1_scales, const uint8_t* w3_codes,
+                      const uint8_t* w3_scales, int32_t E, int32_t I, int32_t H, uint8_t* codes,
+                      uint8_t* scales, void* stream);
+int moe_pack_mxfp4_down(const uint8_t* w2_codes, const uint8_t* w2_scales, int32_t E, int32_t H,
+                        int32_t I, uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
+ * moe_expert_ffn_mxfp4 -- moe_expert_ffn with MXFP4 expert weights, packed by
+ * moe_pack_mxfp4_up (up_codes, up_scales) and moe_pack_mxfp4_down
+ * (down_codes, down_scales):
+ *   y_perm[s, :] = W2_e (silu(W1_e x[t]) * (W3_e x[t]))
+ * with every W the dequantized matrix.  The codes are expanded to bf16 in
+ * registers (exact: an E2M1 value times a power of two in range is a bf16
+ * number) and multiplied exactly as in moe_expert_ffn, so the result equals
+ * moe_expert_ffn's on the dequantized weights.  Each active expert's codes
+ * and scales are streamed once per call when it has at most 32 tokens; a
+ * bigger bucket is split into groups of 32 tokens sharing the XCD's L2.
+ * Other arguments, the workspace (moe_ffn_workspace_bytes) and the error
+ * behaviour are those of moe_expert_ffn; in addition H % 64 == 0 and
+ * I % 64 == 0 (else MOE_ERR_UNSUPPORTED), and the scale pointers must be
+ * 4-byte aligned.  _up and _down are its two halves, as for moe_expert_ffn.
+ */
+int moe_expert_ffn_mxfp4(const float* x, const uint8_t* up_codes, const uint8_t* up_scales,
+                         const uint8_t* down_codes, const uint8_t* down_scales,
+                         const int32_t* offsets, const int32_t* perm_token,
+                         const int32_t* union_ids, const int32_t* union_size, moe_dims d,
+                         float* y_perm, void* ws, size_t ws_bytes, void* stream);
+int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes, const uint8_t* up_scales,
+                            const int32_t* offsets, const int32_t* perm_token,
+                            const int32_t* union_ids, const int32_t* union_size, moe_dims d,
+                            void* ws, size_t ws_bytes, void* stream);
+int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_codes,
+                              const uint8_t* down_scales, const int32_t* offsets,
+                              const int32_t* perm_token, const int32_t* union_ids,
+                              const int32_t* union_size, moe_dims d, size_t ws_bytes,
+                              float* y_perm, void* stream);
+
+/*
  * moe_combine -- weighted unpermute: out[t, :] = sum over j = 0..K-1 (in that
  * order) of topk_w[t, j] * y_perm[pair_pos[t*K + j], :].  Deterministic, no
  * atomics.  y_perm [T*K, H], topk_w [T, K] fp32, pair_pos [T*K] int32

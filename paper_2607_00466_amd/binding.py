@@ -60,6 +60,13 @@ _SIGNATURES = {
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
     "moe_pack_weights": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
                                         _vp]),
+    "moe_pack_mxfp4_up": (ctypes.c_int, [_vp, _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32, _vp, _vp, _vp]),
+    "moe_pack_mxfp4_down": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           _vp, _vp, _vp]),
+    "moe_expert_ffn_mxfp4": (ctypes.c_int, [_vp] * 9 + [MoeDims, _vp, _vp, ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_mxfp4_up": (ctypes.c_int, [_vp] * 7 + [MoeDims, _vp, ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_mxfp4_down": (ctypes.c_int, [_vp] * 7 + [MoeDims, ctypes.c_size_t, _vp, _vp]),
     "moe_sig_capture": (ctypes.c_int, [_vp, _vp] + [ctypes.c_int32] * 7 + [_vp, _vp, _vp]),
     "moe_sig_reset": (ctypes.c_int, [_vp] + [ctypes.c_int32] * 4 + [_vp, _vp]),
     "moe_sig_request_counts": (ctypes.c_int, [_vp, _vp, _vp] + [ctypes.c_int32] * 5 + [_vp, _vp]),
@@ -235,6 +242,106 @@ def pack_expert_weights(w1, w3, w2, stream=None):
     return tuple(moe_pack_weights(w, stream=stream) for w in (w1, w3, w2))
 
 
+# ----------------------------------------------------------------------------- MXFP4 experts
+#
+# An MXFP4 weight is a pair (codes, scales) of uint8 device tensors: codes
+# [E, R, K/2] (two E2M1 codes a byte, the even index in the low nibble) and
+# scales [E, R, K/32] (E8M0), as checkpoints store them; packed pairs are
+# flat uint8 tensors of the same sizes.
+
+def _need_u8(t, name: str, numel: int) -> None:
+    _need(t, name, torch.uint8, numel)
+
+
+def moe_pack_mxfp4_up(w1, w3, stream=None):
+    """Pack W1 and W3 (each (codes [E,I,H/2], scales [E,I,H/32])); returns (codes, scales)."""
+    (c1, s1), (c3, s3) = w1, w3
+    if c1.dim() != 3:
+        raise ValueError("codes: expected [E, R, K/2]")
+    E, I, H = int(c1.shape[0]), int(c1.shape[1]), int(c1.shape[2]) * 2
+    for name, t, n in (("w1 codes", c1, E * I * H // 2), ("w3 codes", c3, E * I * H // 2),
+                       ("w1 scales", s1, E * I * H // 32), ("w3 scales", s3, E * I * H // 32)):
+        _need_u8(t, name, n)
+    codes = torch.empty(E * I * H, dtype=torch.uint8, device=c1.device)
+    scales = torch.empty(E * I * H // 16, dtype=torch.uint8, device=c1.device)
+    _check("moe_pack_mxfp4_up", load().moe_pack_mxfp4_up(
+        _ptr(c1), _ptr(s1), _ptr(c3), _ptr(s3), E, I, H, _ptr(codes), _ptr(scales), _stream(stream)))
+    return codes, scales
+
+
+def moe_pack_mxfp4_down(w2, stream=None):
+    """Pack W2 ((codes [E,H,I/2], scales [E,H,I/32])); returns (codes, scales)."""
+    c2, s2 = w2
+    if c2.dim() != 3:
+        raise ValueError("codes: expected [E, R, K/2]")
+    E, H, I = int(c2.shape[0]), int(c2.shape[1]), int(c2.shape[2]) * 2
+    _need_u8(c2, "w2 codes", E * H * I // 2)
+    _need_u8(s2, "w2 scales", E * H * I // 32)
+    codes = torch.empty(E * H * I // 2, dtype=torch.uint8, device=c2.device)
+    scales = torch.empty(E * H * I // 32, dtype=torch.uint8, device=c2.device)
+    _check("moe_pack_mxfp4_down", load().moe_pack_mxfp4_down(
+        _ptr(c2), _ptr(s2), E, H, I, _ptr(codes), _ptr(scales), _stream(stream)))
+    return codes, scales
+
+
+def pack_mxfp4_expert_weights(w1, w3, w2, stream=None):
+    """Pack MXFP4 (w1, w3, w2) for moe_expert_ffn_mxfp4; returns (up, down) pairs."""
+    return moe_pack_mxfp4_up(w1, w3, stream), moe_pack_mxfp4_down(w2, stream)
+
+
+def _need_mx_up(up, d: MoeDims) -> None:
+    _need_u8(up[0], "up codes", d.E * d.I * d.H)
+    _need_u8(up[1], "up scales", d.E * d.I * d.H // 16)
+
+
+def _need_mx_down(down, d: MoeDims) -> None:
+    _need_u8(down[0], "down codes", d.E * d.H * d.I // 2)
+    _need_u8(down[1], "down scales", d.E * d.H * d.I // 32)
+
+
+def _need_routing(offsets, perm_token, union_ids, union_size, d: MoeDims) -> None:
+    _need(offsets, "offsets", torch.int32, d.E + 1)
+    _need(perm_token, "perm_token", torch.int32, d.T * d.K)
+    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_size, "union_size", torch.int32, 1)
+
+
+def moe_expert_ffn_mxfp4(x, up, down, offsets, perm_token, union_ids, union_size, d: MoeDims,
+                         y_perm, ws, stream=None) -> None:
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need_mx_up(up, d)
+    _need_mx_down(down, d)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_mxfp4", load().moe_expert_ffn_mxfp4(
+        _ptr(x), _ptr(up[0]), _ptr(up[1]), _ptr(down[0]), _ptr(down[1]), _ptr(offsets),
+        _ptr(perm_token), _ptr(union_ids), _ptr(union_size), d, _ptr(y_perm), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def moe_expert_ffn_mxfp4_up(x, up, offsets, perm_token, union_ids, union_size, d: MoeDims, ws,
+                            stream=None) -> None:
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need_mx_up(up, d)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_mxfp4_up", load().moe_expert_ffn_mxfp4_up(
+        _ptr(x), _ptr(up[0]), _ptr(up[1]), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(union_size), d, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moe_expert_ffn_mxfp4_down(ws, down, offsets, perm_token, union_ids, union_size, d: MoeDims,
+                              y_perm, stream=None) -> None:
+    _need_mx_down(down, d)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_mxfp4_down", load().moe_expert_ffn_mxfp4_down(
+        _ptr(ws), _ptr(down[0]), _ptr(down[1]), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(union_size), d, ws_bytes, _ptr(y_perm), _stream(stream)))
+
+
 def moe_combine(y_perm, pair_pos, topk_w, d: MoeDims, out, stream=None) -> None:
     _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
     _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
@@ -301,6 +408,21 @@ def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None
                buf.union_ids, buf.union_size, stream)
     moe_expert_ffn(x, w1, w3, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
                    buf.y_perm, buf.ws, stream)
+    moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
+    return buf.out
+
+
+def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
+    """moe_layer with MXFP4 experts: ``up`` and ``down`` from pack_mxfp4_expert_weights."""
+    if routing is None:
+        moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
+    else:
+        buf.topk_ids.copy_(routing[0])
+        buf.topk_w.copy_(routing[1])
+    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
+               buf.union_ids, buf.union_size, stream)
+    moe_expert_ffn_mxfp4(x, up, down, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
+                         d, buf.y_perm, buf.ws, stream)
     moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
     return buf.out
 

@@ -32,6 +32,12 @@
 // * Experts of the union are dealt to XCDs round-robin (the dispatcher deals
 //   workgroups round-robin over the 8 XCDs), so all of an expert's
 //   workgroups share one L2 for its activations and weights.
+// * Weights come in one of two formats (a template parameter): bf16, or
+//   MXFP4 (FP4 E2M1 codes with one E8M0 scale per 32 values along the
+//   reduction axis, the format the paper serves GPT-OSS-120B in), whose
+//   codes are expanded to bf16 in registers by the gfx950 scaled convert
+//   right before the same MFMAs -- the products are those of the bf16 path
+//   on the dequantized weights, for about a quarter of the bytes.
 #include "common.hpp"
 
 namespace eldr {
@@ -49,15 +55,45 @@ namespace eldr {
 #ifndef ELDR_FFN_DOWN_WAVES
 #define ELDR_FFN_DOWN_WAVES 4
 #endif
+#ifndef ELDR_FFN_FP4_RING
+#define ELDR_FFN_FP4_RING 4
+#endif
+#ifndef ELDR_FFN_FP4_CHUNK
+#define ELDR_FFN_FP4_CHUNK 8
+#endif
 constexpr int kKStep = 32;        // k per MFMA
 constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
-constexpr int kMaxTiles = 4;      // token tiles of 16 per item: at most 64 tokens of an expert
 constexpr int kMaxExpertsPerXcd = (MOE_MAX_E + kNumXcd - 1) / kNumXcd;
 
-// k-steps of weights in flight per wave (the prefetch depth of the ring).
-template <int NT>
+// Weight formats.
+//   kBf16:  packed by moe_pack_weights; a ring slot is one k-step of the
+//           wave's two 16-row tiles, two 1 KB loads.
+//   kMxfp4: packed by moe_pack_mxfp4_up / _down; a ring slot is two k-steps
+//           of the wave's two 16-row tiles: one 1 KB load of FP4 codes (a
+//           lane's 16 bytes are its 8 codes of tile 0 step 0, tile 0 step 1,
+//           tile 1 step 0, tile 1 step 1) and one 64-byte load of their E8M0
+//           scales (a dword per row, its bytes in the same order).  For up the
+//           two tiles are W1's and W3's rows of the band, for down two
+//           adjacent 16-row tiles of W2.
+enum WeightFmt { kBf16 = 0, kMxfp4 = 1 };
+
+template <int FMT>
+__host__ __device__ constexpr int slot_steps() {
+  return FMT == kBf16 ? 1 : 2;
+}
+
+// Token tiles of 16 per item: at most 64 tokens of an expert for bf16, 32
+// for MXFP4 (whose MFMA and LDS work per weight byte is four times bf16's; a
+// larger bucket takes more token groups, served from L2).
+template <int FMT>
+__host__ __device__ constexpr int max_tiles() {
+  return FMT == kBf16 ? 4 : 2;
+}
+
+// Ring slots of weights in flight per wave (the prefetch depth of the ring).
+template <int FMT, int NT>
 __host__ __device__ constexpr int ring_depth() {
-  return NT <= 2 ? ELDR_FFN_RING_SMALL : ELDR_FFN_RING_LARGE;
+  return FMT == kMxfp4 ? ELDR_FFN_FP4_RING : NT <= 2 ? ELDR_FFN_RING_SMALL : ELDR_FFN_RING_LARGE;
 }
 
 // k-steps per staged chunk: a whole number of ring cycles, as many as keep
@@ -68,9 +104,10 @@ __host__ __device__ constexpr int ring_depth() {
 #ifndef ELDR_FFN_CYCLES2
 #define ELDR_FFN_CYCLES2 1
 #endif
-template <int NT>
+template <int FMT, int NT>
 __host__ __device__ constexpr int chunk_steps() {
-  return ring_depth<NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
+  return FMT == kMxfp4 ? ELDR_FFN_FP4_CHUNK
+                       : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
 }
 
 #ifndef ELDR_FFN_MAX_CHUNK
@@ -82,9 +119,9 @@ __host__ __device__ constexpr int min_c(int a, int b) { return a < b ? a : b; }
 
 // Bytes of one LDS staging buffer (two are used, double-buffered): NT * 16
 // token rows of chunk_steps k-steps (128 bytes each) plus 16 bytes of padding.
-template <int NT>
+template <int FMT, int NT>
 __host__ __device__ constexpr int lds_buf_bytes() {
-  return NT * 16 * (128 * chunk_steps<NT>() + 16);
+  return NT * 16 * (128 * chunk_steps<FMT, NT>() + 16);
 }
 
 enum FfnMode { kUp = 0, kDown = 1 };
@@ -116,6 +153,8 @@ struct FfnArgs {
   int extra_groups;            // MULTI: slots per XCD beyond one group per expert, in bands
   int max_groups;              // MULTI: token groups of the largest possible bucket (T)
   int experts;                 // E
+  const u32x4* qcodes;         // MXFP4: packed FP4 codes (up: W1 and W3; down: W2)
+  const uint32_t* qscales;     // MXFP4: packed E8M0 scales
 };
 
 // Rows per workgroup: up -> 16 rows per wave (each wave reads the same 16
@@ -169,6 +208,18 @@ __device__ __forceinline__ void split8_pk(const u32x4& a, const u32x4& b, u32x4&
   lo = u32x4{l0, l1, l2, l3};
 }
 
+// 8 FP4 E2M1 codes (a dword, the first in the low nibble) times the E8M0
+// scale in the low byte of sc, as the 8 bf16 values of an MFMA operand.  The
+// scaled convert multiplies exactly (an E2M1 value has two significant bits)
+// for scale codes 1 .. 252.
+__device__ __forceinline__ u32x4 expand_fp4(uint32_t w, uint32_t sc) {
+  const float x = __uint_as_float((sc & 0xffu) << 23);
+  return u32x4{__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, x, 0)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, x, 1)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, x, 2)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, x, 3))};
+}
+
 // Activations enter the MFMA B operand as a pair of bf16 numbers (high
 // part, rounded remainder).  In LDS, and for h in the workspace, a row of K
 // values is K / 8 groups of 32 bytes: 8 bf16 high parts, then the 8 matching
@@ -176,11 +227,12 @@ __device__ __forceinline__ void split8_pk(const u32x4& a, const u32x4& b, u32x4&
 // from fp32 and splits it on the way into LDS; its epilogue writes h already
 // split, so the down kernel stages h with a plain copy.
 
-template <int MODE, int NT, bool MULTI>
+template <int MODE, int NT, bool MULTI, int FMT>
 __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
   constexpr int kFfnThreads = ffn_threads<MODE>();
-  constexpr int kBuf = lds_buf_bytes<NT>();
-  constexpr int kRing = ring_depth<NT>();
+  constexpr int kBuf = lds_buf_bytes<FMT, NT>();
+  constexpr int kRing = ring_depth<FMT, NT>();
+  constexpr int kSlot = slot_steps<FMT>();  // k-steps per ring slot
   constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
   __shared__ int tok[kGroupTokens];
@@ -205,6 +257,7 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
   const int slots = gridDim.x / kNumXcd;
   const int K = a.kdim;
   const int nk = K / kKStep;
+  const int nslot = nk / kSlot;  // ring slots of a row band
   const int arow = lane & 15;
   const int kgrp = lane >> 4;
   const size_t tiles_per_expert = (size_t)(a.rows / 16);
@@ -230,18 +283,31 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
         a.wa + ((e * tiles_per_expert + ra0 / 16) * nk) * kFragElems + lane * 8;
     const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) +
                           ((e * tiles_per_expert + ra1 / 16) * nk) * kFragElems + lane * 8;
+    // MXFP4: the wave's two tiles are one packed band (up: 16 rows of W1
+    // and W3; down: 32 rows of W2) of nslot slots, 64 code pieces and 16
+    // scale dwords a slot.
+    constexpr int kBandRows = MODE == kUp ? 16 : 32;
+    const size_t qband = (size_t)e * (a.rows / kBandRows) + ra0 / kBandRows;
+    const u32x4* pq = a.qcodes + qband * nslot * 64 + lane;
+    const uint32_t* ps = a.qscales + qband * nslot * 16 + arow;
 
-    // Weight ring: slot i holds the fragments of the k-step congruent to i
-    // mod kRing.  Loads past the last k-step re-read the last one (always
+    // Weight ring: slot i holds the weights of the ring slot congruent to i
+    // mod kRing.  Loads past the last slot re-read the last one (always
     // issued, never used), which keeps the loop free of branches.
-    u32x4 ring0[kRing], ring1[kRing];
-    auto ring_prologue = [&]() {
-#pragma unroll
-      for (int i = 0; i < kRing; ++i) {
-        const int si = min(i, nk - 1);
+    u32x4 ring0[kRing], ring1[kRing];  // MXFP4: ring0 holds the codes
+    uint32_t rsc[kRing];               // MXFP4: the scales
+    auto ring_load = [&](const int i, const int si) {
+      if constexpr (FMT == kBf16) {
         ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)si * kFragElems);
         ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)si * kFragElems);
+      } else {
+        ring0[i] = pq[(size_t)si * 64];
+        rsc[i] = ps[(size_t)si * 16];
       }
+    };
+    auto ring_prologue = [&]() {
+#pragma unroll
+      for (int i = 0; i < kRing; ++i) ring_load(i, min(i, nslot - 1));
     };
 
     ring_prologue();
@@ -254,9 +320,9 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
     // same buffer and a small bucket crosses as few barriers as a large one.
     auto run_pass = [&](auto NTB_) {
       constexpr int NTB = decltype(NTB_)::value;
-      constexpr int kChunk = min_c(chunk_steps<NT>() * NT / NTB, kMaxChunk);
+      constexpr int kChunk = min_c(chunk_steps<FMT, NT>() * NT / NTB, kMaxChunk);
       constexpr int kStride = 128 * kChunk + 16;  // bytes per staged token row: an odd multiple of 16
-      static_assert(kChunk % kRing == 0, "a chunk is a whole number of ring cycles");
+      static_assert(kChunk % (kRing * kSlot) == 0, "a chunk is a whole number of ring cycles");
       static_assert(NTB * 16 * kStride <= kBuf, "a chunk fits its buffer");
       constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
       static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
@@ -317,14 +383,24 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
         acc1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
 
-      // One k-step: multiply ring slot I against the staged tokens of
-      // chunk-relative step s - ks, then refill the slot with step s + kRing.
-      // The refill is issued after the MFMAs that read the slot, into the same
-      // registers, and a scheduling barrier keeps it there, so each slot stays
-      // in place and kRing steps of loads are always in flight.
+      // One k-step: multiply the weights of chunk-relative step I (ring slot
+      // (I / kSlot) mod kRing) against the staged tokens of step s, and after
+      // a slot's last k-step refill it with the slot kRing ahead.  The refill
+      // is issued after the MFMAs that read the slot, into the same
+      // registers, and a scheduling barrier keeps it there, so each slot
+      // stays in place and kRing slots of loads are always in flight.
       auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
-        constexpr int i = decltype(I)::value % kRing;
+        constexpr int i = (decltype(I)::value / kSlot) % kRing;
+        constexpr int j = decltype(I)::value % kSlot;
         const unsigned char* bs = bb + (s - ks) * 128;
+        u32x4 a0, a1;
+        if constexpr (FMT == kBf16) {
+          a0 = ring0[i];
+          a1 = ring1[i];
+        } else {
+          a0 = expand_fp4(ring0[i][j], rsc[i] >> (8 * j));
+          a1 = expand_fp4(ring0[i][2 + j], rsc[i] >> (8 * (2 + j)));
+        }
   #pragma unroll
         for (int t = 0; t < NTB; ++t) {
           if (t < nt) {
@@ -335,15 +411,13 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
             const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * kStride);
             const u32x4 bh = bp[0];
             const u32x4 bl = bp[1];
-            acc0[t] = mfma16x16x32(ring0[i], bh, acc0[t]);
-            acc0[t] = mfma16x16x32(ring0[i], bl, acc0[t]);
-            acc1[t] = mfma16x16x32(ring1[i], bh, acc1[t]);
-            acc1[t] = mfma16x16x32(ring1[i], bl, acc1[t]);
+            acc0[t] = mfma16x16x32(a0, bh, acc0[t]);
+            acc0[t] = mfma16x16x32(a0, bl, acc0[t]);
+            acc1[t] = mfma16x16x32(a1, bh, acc1[t]);
+            acc1[t] = mfma16x16x32(a1, bl, acc1[t]);
           }
         }
-        const int sn = min(s + kRing, nk - 1);
-        ring0[i] = *reinterpret_cast<const u32x4*>(pa0 + (size_t)sn * kFragElems);
-        ring1[i] = *reinterpret_cast<const u32x4*>(pa1 + (size_t)sn * kFragElems);
+        if constexpr (j == kSlot - 1) ring_load(i, min(s / kSlot + kRing, nslot - 1));
         __builtin_amdgcn_sched_barrier(0);
       };
 
@@ -352,8 +426,8 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
       // or itself again), runs kChunk k-steps, unrolled, and publishes the next
       // chunk into the other buffer.  In steady state the staged groups are
       // older than the weight loads behind them, so a publish waits for them
-      // alone.  Chunk starts are multiples of kRing, so step ks + I sits in
-      // ring slot I % kRing.  The buffer published at the end of iteration ch
+      // alone.  Chunk starts are multiples of the ring cycle (kRing slots),
+      // so step ks + I sits in ring slot (I / kSlot) % kRing.  The buffer published at the end of iteration ch
       // was last read in iteration ch - 1, before the previous barrier.
       const int nfull = nk / kChunk;
       const int last_start = ((nk - 1) / kChunk) * kChunk;
@@ -486,36 +560,36 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
 // with more tokens than one item takes also get room for the average number
 // of extra token groups an XCD sees (T*K / (NT*16) extra groups at most in
 // all), and slots loop over any items beyond that.
-template <int MODE, int NT>
+template <int MODE, int FMT, int NT>
 static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
   const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
   if (T <= NT * 16) {
     a.extra_groups = 0;
-    hipLaunchKernelGGL((ffn_kernel<MODE, NT, false>), dim3(kNumXcd * a.tiles * per_xcd),
+    hipLaunchKernelGGL((ffn_kernel<MODE, NT, false, FMT>), dim3(kNumXcd * a.tiles * per_xcd),
                        dim3(ffn_threads<MODE>()), 0, s, a);
   } else {
     const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
     a.extra_groups = extra;
     a.max_groups = (T + NT * 16 - 1) / (NT * 16);
-    hipLaunchKernelGGL((ffn_kernel<MODE, NT, true>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
+    hipLaunchKernelGGL((ffn_kernel<MODE, NT, true, FMT>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
                        dim3(ffn_threads<MODE>()), 0, s, a);
   }
 }
 
 // Token tiles of 16 per item: enough for every bucket when T is small (a
-// bucket never exceeds T tokens), at most kMaxTiles.
-template <int MODE>
+// bucket never exceeds T tokens), at most max_tiles.
+template <int MODE, int FMT>
 static void launch_ffn_nt(const FfnArgs& a, int T, int K, int E, hipStream_t s) {
   int nt_T = T;
 #ifdef ELDR_FFN_FORCE_NT
   nt_T = 16 * ELDR_FFN_FORCE_NT;
 #endif
   if (nt_T <= 16)
-    launch_ffn<MODE, 1>(a, T, K, E, s);
+    launch_ffn<MODE, FMT, 1>(a, T, K, E, s);
   else if (nt_T <= 32)
-    launch_ffn<MODE, 2>(a, T, K, E, s);
+    launch_ffn<MODE, FMT, 2>(a, T, K, E, s);
   else
-    launch_ffn<MODE, kMaxTiles>(a, T, K, E, s);
+    launch_ffn<MODE, FMT, max_tiles<FMT>()>(a, T, K, E, s);
 }
 
 }  // namespace eldr
@@ -554,9 +628,9 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint1
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w1, w3, offsets, perm_token, union_ids,
-                   union_size, ws, d.I, d.H, 0, 0, 1, d.E};
+                   union_size, ws, d.I, d.H, 0, 0, 1, d.E, nullptr, nullptr};
   up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
-  eldr::launch_ffn_nt<eldr::kUp>(up, d.T, d.K, d.E, s);
+  eldr::launch_ffn_nt<eldr::kUp, eldr::kBf16>(up, d.T, d.K, d.E, s);
   return launch_status();
 }
 
@@ -574,10 +648,11 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, nullptr, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E};
+                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E, nullptr, nullptr};
   down.tiles =
       (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
-  eldr::launch_ffn_nt<eldr::kDown>(down, d.T, d.K, d.E, reinterpret_cast<hipStream_t>(stream));
+  eldr::launch_ffn_nt<eldr::kDown, eldr::kBf16>(down, d.T, d.K, d.E,
+                                               reinterpret_cast<hipStream_t>(stream));
   return launch_status();
 }
 
@@ -603,4 +678,94 @@ extern "C" int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t
   if (st != MOE_OK) return st;
   return moe_expert_ffn_down(h, w2, offsets, perm_token, union_ids, union_size, d, ws_bytes,
                              y_perm, stream);
+}
+
+// ---- MXFP4 expert weights ----------------------------------------------------
+
+namespace {
+
+int check_mxfp4_dims(const moe_dims& d) {
+  const int st = eldr_host::check_dims(d);
+  if (st != MOE_OK) return st;
+  // a ring slot is two k-steps (64 values) of both reductions
+  if (d.H % 64 != 0 || d.I % 64 != 0) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes,
+                                       const uint8_t* up_scales, const int32_t* offsets,
+                                       const int32_t* perm_token, const int32_t* union_ids,
+                                       const int32_t* union_size, moe_dims d, void* ws,
+                                       size_t ws_bytes, void* stream) {
+  using namespace eldr_host;
+  int st = check_mxfp4_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0) return MOE_OK;
+  if (!x || !up_codes || !up_scales || !ws) return MOE_ERR_INVALID;
+  st = check_ffn_common(d, offsets, perm_token, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(up_codes) || !aligned4(up_scales) || !aligned16(ws))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, nullptr, offsets, perm_token,
+                   union_ids, union_size, ws, d.I, d.H, 0, 0, 1, d.E,
+                   reinterpret_cast<const eldr::u32x4*>(up_codes),
+                   reinterpret_cast<const uint32_t*>(up_scales)};
+  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
+  eldr::launch_ffn_nt<eldr::kUp, eldr::kMxfp4>(up, d.T, d.K, d.E,
+                                              reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_codes,
+                                         const uint8_t* down_scales, const int32_t* offsets,
+                                         const int32_t* perm_token, const int32_t* union_ids,
+                                         const int32_t* union_size, moe_dims d, size_t ws_bytes,
+                                         float* y_perm, void* stream) {
+  using namespace eldr_host;
+  int st = check_mxfp4_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0) return MOE_OK;
+  if (!ws || !down_codes || !down_scales || !y_perm) return MOE_ERR_INVALID;
+  st = check_ffn_common(d, offsets, perm_token, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(ws) || !aligned16(down_codes) || !aligned4(down_scales) || !aligned16(y_perm))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), nullptr, nullptr, offsets, perm_token,
+                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E,
+                     reinterpret_cast<const eldr::u32x4*>(down_codes),
+                     reinterpret_cast<const uint32_t*>(down_scales)};
+  down.tiles =
+      (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
+  eldr::launch_ffn_nt<eldr::kDown, eldr::kMxfp4>(down, d.T, d.K, d.E,
+                                                reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" int moe_expert_ffn_mxfp4(const float* x, const uint8_t* up_codes,
+                                    const uint8_t* up_scales, const uint8_t* down_codes,
+                                    const uint8_t* down_scales, const int32_t* offsets,
+                                    const int32_t* perm_token, const int32_t* union_ids,
+                                    const int32_t* union_size, moe_dims d, float* y_perm, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  using namespace eldr_host;
+  int st = check_mxfp4_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0) return MOE_OK;
+  if (!x || !up_codes || !up_scales || !down_codes || !down_scales || !y_perm || !ws)
+    return MOE_ERR_INVALID;
+  st = check_ffn_common(d, offsets, perm_token, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(up_codes) || !aligned4(up_scales) || !aligned16(down_codes) ||
+      !aligned4(down_scales) || !aligned16(y_perm) || !aligned16(ws))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  st = moe_expert_ffn_mxfp4_up(x, up_codes, up_scales, offsets, perm_token, union_ids, union_size,
+                               d, ws, ws_bytes, stream);
+  if (st != MOE_OK) return st;
+  return moe_expert_ffn_mxfp4_down(ws, down_codes, down_scales, offsets, perm_token, union_ids,
+                                   union_size, d, ws_bytes, y_perm, stream);
 }

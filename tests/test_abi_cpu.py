@@ -151,3 +151,42 @@ def test_stream_probe_validates_on_host(lib):
     assert lib.moe_stream_read_probe(None, 64, FAKE, None) == B.MOE_ERR_INVALID
     assert lib.moe_stream_read_probe(FAKE, 24, FAKE, None) == B.MOE_ERR_UNSUPPORTED
     assert lib.moe_stream_read_probe(FAKE_MIS, 64, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+
+
+def test_mxfp4_calls_validate_on_host(lib):
+    ffn, up, down = lib.moe_expert_ffn_mxfp4, lib.moe_expert_ffn_mxfp4_up, lib.moe_expert_ffn_mxfp4_down
+    d = B.dims(64, 2880, 128, 4, 2880)
+    need = B.moe_ffn_workspace_bytes(d)
+    args9 = [FAKE] * 9
+    # H or I not a multiple of 64 (the MXFP4 slot), though multiples of 32
+    for bad in (B.dims(64, 2880 + 32, 128, 4, 2880), B.dims(64, 2880, 128, 4, 2880 - 32)):
+        assert ffn(*args9, bad, FAKE, FAKE, 1 << 40, None) == B.MOE_ERR_UNSUPPORTED
+        assert up(*[FAKE] * 7, bad, FAKE, 1 << 40, None) == B.MOE_ERR_UNSUPPORTED
+        assert down(*[FAKE] * 7, bad, 1 << 40, FAKE, None) == B.MOE_ERR_UNSUPPORTED
+    # null pointers, misaligned codes, a small workspace
+    assert ffn(FAKE, None, *[FAKE] * 7, d, FAKE, FAKE, need, None) == B.MOE_ERR_INVALID
+    assert ffn(*args9, d, None, FAKE, need, None) == B.MOE_ERR_INVALID
+    assert ffn(FAKE, FAKE_MIS, *[FAKE] * 7, d, FAKE, FAKE, need, None) == B.MOE_ERR_UNSUPPORTED
+    odd = ctypes.c_void_p(0x10001)
+    assert ffn(FAKE, FAKE, odd, *[FAKE] * 6, d, FAKE, FAKE, need, None) == B.MOE_ERR_UNSUPPORTED
+    assert ffn(*args9, d, FAKE, FAKE, need - 1, None) == B.MOE_ERR_WORKSPACE
+    assert up(*[FAKE] * 7, d, FAKE, need - 1, None) == B.MOE_ERR_WORKSPACE
+    assert down(FAKE, None, *[FAKE] * 5, d, need, FAKE, None) == B.MOE_ERR_INVALID
+    # an empty batch launches nothing and touches no pointer
+    d0 = B.dims(0, 2880, 128, 4, 2880)
+    assert ffn(*[None] * 9, d0, None, None, 0, None) == B.MOE_OK
+
+
+def test_mxfp4_pack_arguments_rejected(lib):
+    pu, pd = lib.moe_pack_mxfp4_up, lib.moe_pack_mxfp4_down
+    F2 = ctypes.c_void_p(0x20000)
+    F3 = ctypes.c_void_p(0x30000)
+    assert pu(FAKE, FAKE, FAKE, FAKE, -1, 16, 64, F2, F3, None) == B.MOE_ERR_INVALID
+    assert pu(FAKE, FAKE, FAKE, FAKE, 2, 24, 64, F2, F3, None) == B.MOE_ERR_UNSUPPORTED   # I % 16
+    assert pu(FAKE, FAKE, FAKE, FAKE, 2, 16, 96, F2, F3, None) == B.MOE_ERR_UNSUPPORTED   # H % 64
+    assert pd(FAKE, FAKE, 2, 48, 64, F2, F3, None) == B.MOE_ERR_UNSUPPORTED               # H % 32
+    assert pd(FAKE, FAKE, 2, 32, 96, F2, F3, None) == B.MOE_ERR_UNSUPPORTED               # I % 64
+    assert pu(FAKE, None, FAKE, FAKE, 2, 16, 64, F2, F3, None) == B.MOE_ERR_INVALID
+    assert pd(FAKE, FAKE, 2, 32, 64, FAKE, F3, None) == B.MOE_ERR_INVALID                 # in place
+    assert pd(FAKE, FAKE, 2, 32, 64, FAKE_MIS, F3, None) == B.MOE_ERR_UNSUPPORTED         # codes out
+    assert pu(FAKE, FAKE, FAKE, FAKE, 0, 16, 64, None, None, None) == B.MOE_OK            # nothing to do

@@ -1,0 +1,237 @@
+"""GPU parity of the MXFP4 expert path against the dequantizing oracle.
+
+The MXFP4 FFN expands FP4 codes to bf16 in registers and then multiplies as
+the bf16 FFN does, so besides the oracle comparison (float64 on the
+dequantized weights) it must equal the bf16 path run on the dequantized
+weights bit for bit.  The packed layouts are checked against the permutation
+the header documents, written out here with NumPy.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from oracle import mxfp4 as MX
+from paper_2607_00466_amd import binding as B
+from paper_2607_00466_amd import synth
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+GPTOSS = synth.SHAPES["gpt_oss_120b"]
+
+
+class MxLayer:
+    """One layer with MXFP4 experts on the device, plus host copies for the oracle."""
+
+    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0, q=None):
+        self.shape, self.T = shape, T
+        self.x_np = synth.hidden_states(T, shape.H, seed)
+        self.wg_np = synth.gate_weights(shape, seed)
+        self.x = torch.from_numpy(self.x_np).cuda()
+        self.wg = torch.from_numpy(self.wg_np).cuda()
+        self.q = q if q is not None else synth.mxfp4_expert_weights(shape, seed, device="cuda")
+        self.up, self.down = B.pack_mxfp4_expert_weights(self.q["w1"], self.q["w3"], self.q["w2"])
+        self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        self.buf = B.LayerBuffers.allocate(self.d)
+
+    def host_q(self, experts=None):
+        """{name: (codes, scales)} as NumPy, all experts or only the listed ones (others zero)."""
+        out = {}
+        for name, (c, s) in self.q.items():
+            if experts is None:
+                out[name] = (c.cpu().numpy(), s.cpu().numpy())
+                continue
+            hc = np.zeros(tuple(c.shape), np.uint8)
+            hs = np.full(tuple(s.shape), 127, np.uint8)
+            for e in experts:
+                hc[e] = c[e].cpu().numpy()
+                hs[e] = s[e].cpu().numpy()
+            out[name] = (hc, hs)
+        return out
+
+    def run(self, routing=None):
+        if routing is not None:
+            routing = (torch.from_numpy(np.ascontiguousarray(routing[0], np.int32)).cuda(),
+                       torch.from_numpy(np.ascontiguousarray(routing[1], np.float32)).cuda())
+        B.moe_layer_mxfp4(self.x, self.wg, self.up, self.down, self.d, self.buf, routing=routing)
+        torch.cuda.synchronize()
+        return G.fetch(self.buf, self.d)
+
+
+def _check_layer(layer: MxLayer, g: dict, routing=None) -> None:
+    s = layer.shape
+    if routing is None:
+        G.check_gate(g, layer.x_np, layer.wg_np, s.K)
+        ids, wts = g["ids"].astype(np.int64), g["weights"]
+    else:
+        ids, wts = routing
+    G.compare_buckets(g, ids, s.E)
+    q = layer.host_q()
+    b = O.bucket(ids, s.E)
+    y = MX.expert_ffn(layer.x_np, q["w1"], q["w3"], q["w2"], ids, b)
+    G.check_output(g["y_slots"], y, "MXFP4 expert FFN per slot")
+    out = O.combine(y, b["pair_pos"], np.asarray(wts, np.float64))
+    G.check_output(g["out"], out, "MXFP4 layer output")
+
+
+# ---------------------------------------------------------------------------- packing
+
+def _dwords(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a).view(np.uint32)
+
+
+@pytest.mark.parametrize("E,I,H", [(3, 64, 64), (2, 192, 320), (4, 2880, 2880)])
+def test_pack_mxfp4_is_the_documented_permutation(E, I, H):
+    G.say(f"case: MXFP4 pack E={E} I={I} H={H}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(E * 7919 + I)
+    rnd = lambda *shape: torch.randint(0, 256, shape, generator=g, device="cuda", dtype=torch.int32).to(torch.uint8)
+    w1, w3 = (rnd(E, I, H // 2), rnd(E, I, H // 32)), (rnd(E, I, H // 2), rnd(E, I, H // 32))
+    w2 = (rnd(E, H, I // 2), rnd(E, H, I // 32))
+    (uc, us), (dc, ds) = B.pack_mxfp4_expert_weights(w1, w3, w2)
+    torch.cuda.synchronize()
+    h = lambda t: t.cpu().numpy()
+    # up codes: per (expert, 16-row band, slot of 2 k-steps), lane = 16 g + r holds the dwords
+    # (W1 step 0, W1 step 1, W3 step 0, W3 step 1) of row r, k-group g
+    ns = H // 64
+    parts = [_dwords(h(c)).reshape(E, I // 16, 16, ns, 2, 4) for c in (w1[0], w3[0])]
+    ref = np.stack([p.transpose(0, 1, 3, 5, 2, 4) for p in parts], axis=-2)  # [E,nb,ns,g,r,m,j]
+    assert np.array_equal(_dwords(h(uc)), ref.reshape(-1))
+    parts = [h(s).reshape(E, I // 16, 16, ns, 2) for s in (w1[1], w3[1])]
+    ref = np.stack([p.transpose(0, 1, 3, 2, 4) for p in parts], axis=-2)       # [E,nb,ns,r,m,j]
+    assert np.array_equal(h(us), ref.reshape(-1))
+    # down: the two 16-row halves of each 32-row band of W2
+    ns = I // 64
+    p = _dwords(h(w2[0])).reshape(E, H // 32, 2, 16, ns, 2, 4)
+    ref = p.transpose(0, 1, 4, 6, 3, 2, 5)                                      # [E,nb,ns,g,r,m,j]
+    assert np.array_equal(_dwords(h(dc)), ref.reshape(-1))
+    p = h(w2[1]).reshape(E, H // 32, 2, 16, ns, 2)
+    assert np.array_equal(h(ds), p.transpose(0, 1, 4, 3, 2, 5).reshape(-1))
+
+
+# ---------------------------------------------------------------------------- FFN parity
+
+@pytest.mark.parametrize("E,K,H,I,T", [
+    (8, 2, 192, 320, 8),      # one token tile; up: a lone tail chunk, down: a partial row band
+    (8, 2, 192, 320, 24),     # two token tiles
+    (6, 3, 256, 128, 100),    # token groups of 32 (buckets above 32 tokens)
+    (4, 2, 2880, 2880, 40),   # full-size reductions: 11 whole chunks and a tail
+])
+def test_mxfp4_layer_matches_oracle(E, K, H, I, T):
+    G.say(f"case: MXFP4 layer E={E} top-{K} H={H} I={I} T={T}, gate-routed")
+    layer = MxLayer(synth.LayerShape("mx", E=E, K=K, H=H, I=I), T, seed=E + T)
+    _check_layer(layer, layer.run())
+
+
+def test_mxfp4_full_code_and_scale_range():
+    # random codes over all 16 E2M1 values (signed zeros, subnormal 0.5, +-6) and
+    # scale codes spread over 41 binades, on every expert
+    G.say("case: MXFP4 random codes, scale codes 100..140, E=6 top-2 H=128 I=192 T=20")
+    sh = synth.LayerShape("mx_range", E=6, K=2, H=128, I=192)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    rnd = lambda lo, hi, *shape: torch.randint(lo, hi, shape, generator=g, device="cuda",
+                                               dtype=torch.int32).to(torch.uint8)
+    q = {"w1": (rnd(0, 256, 6, 192, 64), rnd(100, 141, 6, 192, 4)),
+         "w3": (rnd(0, 256, 6, 192, 64), rnd(100, 141, 6, 192, 4)),
+         "w2": (rnd(0, 256, 6, 128, 96), rnd(100, 141, 6, 128, 6))}
+    layer = MxLayer(sh, 20, seed=5, q=q)
+    ids, w, _ = synth.controlled_routing(20, 6, 2, U=6, seed=5)
+    g = layer.run((ids, w))
+    G.compare_buckets(g, ids, sh.E)
+    qh = layer.host_q()
+    b = O.bucket(ids, sh.E)
+    with np.errstate(over="ignore"):
+        y = MX.expert_ffn(layer.x_np, qh["w1"], qh["w3"], qh["w2"], ids, b)
+    # outputs reach 1e14 here, so the absolute MAE bar is replaced by its
+    # scale-free form (MAE relative to the mean output magnitude)
+    nw, mae = G.output_errors(g["y_slots"], y)
+    rel_mae = mae / np.abs(y).mean()
+    G.say(f"  normwise max rel err {nw:.3e}, MAE / mean|ref| {rel_mae:.3e}")
+    assert nw <= G.OUT_NORMWISE_DESIGN and rel_mae <= G.OUT_MAE
+
+
+def test_mxfp4_equals_bf16_path_on_dequantized_weights():
+    G.say("case: MXFP4 vs bf16 path on the dequantized weights, E=6 top-3 H=256 I=128 T=100")
+    sh = synth.LayerShape("mx_eq", E=6, K=3, H=256, I=128)
+    layer = MxLayer(sh, 100, seed=3)
+    g = layer.run()
+    q = layer.host_q()
+    bf = []
+    for name in ("w1", "w3", "w2"):
+        wf = MX.dequantize(*q[name]).astype(np.float32)     # exact: every value is a bf16 number
+        assert not (wf.view(np.uint32) & 0xFFFF).any()
+        bf.append(torch.from_numpy(wf).cuda().to(torch.bfloat16))
+    p1, p3, p2 = B.pack_expert_weights(*bf)
+    buf = B.LayerBuffers.allocate(layer.d)
+    B.moe_layer(layer.x, layer.wg, p1, p3, p2, layer.d, buf)
+    torch.cuda.synchronize()
+    r = G.fetch(buf, layer.d)
+    assert np.array_equal(r["ids"], g["ids"])
+    assert np.array_equal(r["y_slots"], g["y_slots"]), "MXFP4 and bf16 paths differ"
+    assert np.array_equal(r["out"], g["out"])
+
+
+def test_mxfp4_big_buckets_take_token_groups():
+    G.say("case: MXFP4 200 tokens on 8 of 16 experts (buckets of ~50), H=256 I=192")
+    sh = synth.LayerShape("mx_big", E=16, K=2, H=256, I=192)
+    layer = MxLayer(sh, 200, seed=8)
+    ids, w, _ = synth.controlled_routing(200, 16, 2, U=8, seed=8)
+    g = layer.run((ids, w))
+    G.say(f"  max bucket {g['counts'].max()}")
+    assert g["counts"].max() > 32
+    _check_layer(layer, g, (ids, w))
+
+
+def test_mxfp4_empty_batch_and_invalid_routing():
+    G.say("case: MXFP4 empty batch, then a duplicated id (invalid routing)")
+    sh = synth.LayerShape("mx_edge", E=8, K=2, H=128, I=64)
+    layer = MxLayer(sh, 6, seed=2)
+    d0 = B.dims(0, sh.H, sh.E, sh.K, sh.I)
+    B.moe_expert_ffn_mxfp4(layer.x, layer.up, layer.down, layer.buf.offsets, layer.buf.perm_token,
+                           layer.buf.union_ids, layer.buf.union_size, d0, layer.buf.y_perm,
+                           layer.buf.ws)
+    ids = np.array([[0, 1], [2, 2], [3, 4], [5, 6], [7, 0], [1, 2]], np.int32)  # token 1 repeats 2
+    w = np.full((6, 2), 0.5, np.float32)
+    layer.buf.y_perm.fill_(123.0)
+    g = layer.run((ids, w))
+    assert g["union_size"] == -1
+    assert np.all(g["y_slots"] == 123.0), "the FFN wrote outputs for invalid routing"
+
+
+# ---------------------------------------------------------------------------- full gpt-oss shape
+
+@pytest.fixture(scope="module")
+def gpt_oss_mx():
+    G.say("building the gpt-oss-shaped MXFP4 layer (E=128 top-4 H=I=2880), T=256")
+    return MxLayer(GPTOSS, 256)
+
+
+def _sampled(layer: MxLayer, g: dict, ids, wts, sample, label):
+    experts = sorted(set(np.asarray(ids)[sample].ravel().tolist()))
+    q = layer.host_q(experts)
+    sub = MX.moe_layer_routed(layer.x_np[sample], np.asarray(ids)[sample],
+                              np.asarray(wts, np.float64)[sample], q["w1"], q["w3"], q["w2"], GPTOSS.E)
+    G.check_output(g["out"][sample], sub["out"], label)
+
+
+def test_gpt_oss_mxfp4_gate_routed_sampled(gpt_oss_mx):
+    G.say("case: gpt-oss MXFP4 layer T=256, gate-routed, sampled tokens")
+    g = gpt_oss_mx.run()
+    G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
+    near = G.check_gate(g, gpt_oss_mx.x_np, gpt_oss_mx.wg_np, GPTOSS.K)
+    ids = g["ids"].astype(np.int64)
+    G.compare_buckets(g, ids, GPTOSS.E)
+    sample = [t for t in (0, 93, 200, 255) if not near[t]]
+    _sampled(gpt_oss_mx, g, ids, g["weights"], sample, "sampled tokens")
+
+
+@pytest.mark.parametrize("U", [32, 128])
+def test_gpt_oss_mxfp4_controlled_union_sampled(gpt_oss_mx, U):
+    G.say(f"case: gpt-oss MXFP4 layer T=256, controlled union U={U}, sampled tokens")
+    ids, w, _ = synth.controlled_routing(256, GPTOSS.E, GPTOSS.K, U=U, seed=U)
+    g = gpt_oss_mx.run((ids, w))
+    G.compare_buckets(g, ids, GPTOSS.E)
+    G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
+    _sampled(gpt_oss_mx, g, ids, w, [3, 130, 254], f"sampled tokens, U={U}")
