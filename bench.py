@@ -81,6 +81,21 @@ def up_bytes(shape: synth.LayerShape, T: int, U: int) -> int:
     return U * 2 * shape.H * shape.I * 2 + 4 * T * shape.H
 
 
+def mx_matrix_bytes(shape: synth.LayerShape) -> int:
+    """MXFP4 bytes of one H x I expert matrix: half a byte a value, one scale byte per 32."""
+    return shape.H * shape.I // 2 + shape.H * shape.I // 32
+
+
+def mx_layer_bytes(shape: synth.LayerShape, T: int, U: int, gate: bool) -> int:
+    """layer_bytes with MXFP4 experts (codes and scales of W1, W3, W2)."""
+    return layer_bytes(shape, T, U, gate) - U * shape.expert_bytes + U * 3 * mx_matrix_bytes(shape)
+
+
+def mx_up_bytes(shape: synth.LayerShape, T: int, U: int) -> int:
+    """Algorithmic bytes of one MXFP4 up launch: W1 and W3 codes and scales of the union, and x."""
+    return U * 2 * mx_matrix_bytes(shape) + 4 * T * shape.H
+
+
 class Bench:
     def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0):
         self.shape = shape
@@ -172,6 +187,148 @@ class Bench:
         down = np.array([e[1].elapsed_time(e[2]) for e in evs])
         return {"layer_ms": layer_ms, "up_ms": float(up.mean()), "down_ms": float(down.mean()),
                 "up_ms_median": float(np.median(up)), "down_ms_median": float(np.median(down))}
+
+
+class MxBench(Bench):
+    """Bench with MXFP4 experts (packed by moe_pack_mxfp4_up / _down)."""
+
+    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0):
+        self.shape = shape
+        self.T = T
+        self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        self.x = torch.from_numpy(synth.hidden_states(T, shape.H, seed)).cuda()
+        self.wg = torch.from_numpy(synth.gate_weights(shape, seed)).cuda()
+        q = synth.mxfp4_expert_weights(shape, seed, device="cuda")
+        self.weights = [B.pack_mxfp4_expert_weights(q["w1"], q["w3"], q["w2"])]
+        del q
+        self.buf = B.LayerBuffers.allocate(self.d)
+        self.stream = torch.cuda.current_stream()
+
+    def rotate(self, union_bytes: int) -> None:
+        R = min(16, max(2, math.ceil(ROTATE_BYTES / max(1, union_bytes))))
+        while len(self.weights) < R:
+            self.weights.append(tuple((c.clone(), s.clone()) for c, s in self.weights[0]))
+
+    def step(self, i: int, routing=None, ev=None) -> None:
+        up, down = self.weights[i % len(self.weights)]
+        d, b = self.d, self.buf
+        if routing is None:
+            B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
+        else:
+            b.topk_ids.copy_(routing[0])
+            b.topk_w.copy_(routing[1])
+        B.moe_bucket(b.topk_ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
+                     b.union_size)
+        if ev is not None:
+            ev[0].record(self.stream)
+        B.moe_expert_ffn_mxfp4_up(self.x, up, b.offsets, b.perm_token, b.union_ids, b.union_size,
+                                  d, b.ws)
+        if ev is not None:
+            ev[1].record(self.stream)
+        B.moe_expert_ffn_mxfp4_down(b.ws, down, b.offsets, b.perm_token, b.union_ids, b.union_size,
+                                    d, b.y_perm)
+        if ev is not None:
+            ev[2].record(self.stream)
+        B.moe_combine(b.y_perm, b.pair_pos, b.topk_w, d, b.out)
+
+
+def mxfp4_workload(path: str, steps: int, warmup: int, layers: int = 36,
+                   cases=(None, 32, 128), formats=("mxfp4", "bf16")) -> None:
+    """One gpt-oss-120b-shaped layer (E=128, top-4, H=I=2880), T=256, with MXFP4
+    experts beside the same layer with bf16 experts: gate-routed and controlled
+    unions 32 and 128.  Then a decode step of ``layers`` distinct MXFP4 layers,
+    all resident (1.7 GB each), gate-routed."""
+    shape = synth.SHAPES["gpt_oss_120b"]
+    T = 256
+    res = {}
+    with open(path, "a") as f:
+        for fmt, cls in (("mxfp4", MxBench), ("bf16", Bench)):
+            if fmt not in formats:
+                continue
+            bench = cls(shape, T)
+            for U in cases:
+                routing = None
+                if U is not None:
+                    ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0)
+                    routing = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
+                bench.step(0, routing)
+                Ur = bench.union()
+                ebytes = 3 * mx_matrix_bytes(shape) if fmt == "mxfp4" else shape.expert_bytes
+                bench.rotate(Ur * ebytes)
+                r = bench.time(steps, warmup, routing)
+                lb = (mx_layer_bytes if fmt == "mxfp4" else layer_bytes)(shape, T, Ur, U is None)
+                ub = (mx_up_bytes if fmt == "mxfp4" else up_bytes)(shape, T, Ur)
+                rec = {"workload": "gpt_oss_120b moe layer, T=256", "experts": fmt,
+                       "routing": "gate" if U is None else f"controlled U={U}", "U": Ur,
+                       "layer_us": r["layer_ms"] * 1e3, "up_us": r["up_ms"] * 1e3,
+                       "down_us": r["down_ms"] * 1e3, "layer_bytes": lb,
+                       "layer_GBps": lb / r["layer_ms"] / 1e6,
+                       "up_GBps": ub / r["up_ms"] / 1e6,
+                       "weight_copies": len(bench.weights)}
+                rec["layer_frac_of_hbm_peak"] = rec["layer_GBps"] / HBM_PEAK_GBS
+                rec["up_frac_of_hbm_peak"] = rec["up_GBps"] / HBM_PEAK_GBS
+                res[(fmt, U)] = rec
+                f.write(json.dumps(rec) + "\n")
+                f.flush()
+                log(f"gpt-oss {fmt} {rec['routing']}: U={Ur} layer {rec['layer_us']:.1f} us "
+                    f"({rec['layer_GBps']:.0f} GB/s), up {rec['up_us']:.1f} us ({rec['up_GBps']:.0f} GB/s), "
+                    f"down {rec['down_us']:.1f} us")
+            del bench
+            torch.cuda.empty_cache()
+        for U in cases if len(formats) == 2 else ():
+            a, b = res[("mxfp4", U)], res[("bf16", U)]
+            f.write(json.dumps({"workload": "gpt_oss_120b moe layer, T=256", "summary": True,
+                                "routing": a["routing"], "U": a["U"],
+                                "mxfp4_speedup_over_bf16": b["layer_us"] / a["layer_us"],
+                                "byte_ratio": b["layer_bytes"] / a["layer_bytes"]}) + "\n")
+        if layers <= 0:
+            return
+        # a whole decode step of distinct MXFP4 layers, every layer resident
+        d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+        lay = []
+        for l in range(layers):
+            q = synth.mxfp4_expert_weights(shape, 0, l, device="cuda")
+            packed = B.pack_mxfp4_expert_weights(q["w1"], q["w3"], q["w2"])
+            del q
+            x = torch.from_numpy(synth.hidden_states(T, shape.H, 0, l)).cuda()
+            wg = torch.from_numpy(synth.gate_weights(shape, 0, l)).cuda()
+            lay.append((x, wg, packed, B.LayerBuffers.allocate(d)))
+        torch.cuda.synchronize()
+        log(f"gpt-oss mxfp4: {layers} layers resident")
+
+        def run_step():
+            for x, wg, (up, down), buf in lay:
+                B.moe_layer_mxfp4(x, wg, up, down, d, buf)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            run_step()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run_step()
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        unions = [int(buf.union_size.item()) for *_, buf in lay]
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(5):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / 5
+        step_bytes = sum(mx_layer_bytes(shape, T, u, True) for u in unions)
+        rec = {"workload": f"gpt_oss_120b x{layers} layers (all resident), T=256, MXFP4 experts",
+               "routing": "gate", "step_ms": ms, "mean_union": float(np.mean(unions)),
+               "step_GBps": step_bytes / ms / 1e6}
+        f.write(json.dumps(rec) + "\n")
+        log(f"gpt-oss mxfp4 x{layers}: {ms:.3f} ms/step, mean union {rec['mean_union']:.1f}, "
+            f"{rec['step_GBps']:.0f} GB/s")
+        del g, lay
+        torch.cuda.empty_cache()
 
 
 def calibration(reps: int = 10) -> dict:
@@ -625,6 +782,16 @@ def main() -> int:
     ap.add_argument("--multilayer", default="",
                     help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
                          "appending JSON lines to this file")
+    ap.add_argument("--mxfp4", default="",
+                    help="also run the gpt-oss-shaped layer with MXFP4 experts beside bf16 experts "
+                         "and a 36-layer MXFP4 step, appending JSON lines to this file")
+    ap.add_argument("--mxfp4-only", action="store_true",
+                    help="run only the --mxfp4 measurement (no layer bench line)")
+    ap.add_argument("--mxfp4-cases", default="gate,32,128",
+                    help="routings of the --mxfp4 layer: 'gate' and/or controlled union sizes")
+    ap.add_argument("--mxfp4-formats", default="mxfp4,bf16", help="expert formats of the --mxfp4 layer")
+    ap.add_argument("--mxfp4-layers", type=int, default=36,
+                    help="layers of the --mxfp4 multi-layer step (0 to skip it)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -634,6 +801,11 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     B.load()
+    mx_args = dict(layers=args.mxfp4_layers, formats=tuple(args.mxfp4_formats.split(",")),
+                   cases=tuple(None if c == "gate" else int(c) for c in args.mxfp4_cases.split(",")))
+    if args.mxfp4_only:
+        mxfp4_workload(args.mxfp4 or "mxfp4.jsonl", args.steps, args.warmup, **mx_args)
+        return 0
     if args.signature_only:
         signature_workload(args.signature or "signature.jsonl")
         if args.routing:
@@ -692,6 +864,8 @@ def main() -> int:
     if args.multilayer:
         domain_workload(args.multilayer, 10, 2)
         gpt_oss_workload(args.multilayer, 5, 1)
+    if args.mxfp4:
+        mxfp4_workload(args.mxfp4, max(20, args.steps // 2), args.warmup, **mx_args)
     print(json.dumps(out), flush=True)
     return 0
 

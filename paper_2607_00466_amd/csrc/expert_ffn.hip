@@ -56,10 +56,13 @@ namespace eldr {
 #define ELDR_FFN_DOWN_WAVES 4
 #endif
 #ifndef ELDR_FFN_FP4_RING
-#define ELDR_FFN_FP4_RING 4
+#define ELDR_FFN_FP4_RING 8
 #endif
 #ifndef ELDR_FFN_FP4_CHUNK
 #define ELDR_FFN_FP4_CHUNK 8
+#endif
+#ifndef ELDR_FFN_FP4_MAX_CHUNK
+#define ELDR_FFN_FP4_MAX_CHUNK 16
 #endif
 constexpr int kKStep = 32;        // k per MFMA
 constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
@@ -90,7 +93,9 @@ __host__ __device__ constexpr int max_tiles() {
   return FMT == kBf16 ? 4 : 2;
 }
 
-// Ring slots of weights in flight per wave (the prefetch depth of the ring).
+// Ring slots of weights in flight per wave (the prefetch depth of the ring;
+// for MXFP4 the most a pass shape uses: a pass never keeps more than one
+// staged chunk of slots in flight).
 template <int FMT, int NT>
 __host__ __device__ constexpr int ring_depth() {
   return FMT == kMxfp4 ? ELDR_FFN_FP4_RING : NT <= 2 ? ELDR_FFN_RING_SMALL : ELDR_FFN_RING_LARGE;
@@ -104,9 +109,11 @@ __host__ __device__ constexpr int ring_depth() {
 #ifndef ELDR_FFN_CYCLES2
 #define ELDR_FFN_CYCLES2 1
 #endif
+// MXFP4 moves a quarter of bf16's bytes per k-step, so it needs longer
+// chunks for the same bytes in flight: 16 token rows of 16 k-steps, or 32 of 8.
 template <int FMT, int NT>
 __host__ __device__ constexpr int chunk_steps() {
-  return FMT == kMxfp4 ? ELDR_FFN_FP4_CHUNK
+  return FMT == kMxfp4 ? (NT == 1 ? 2 : 1) * ELDR_FFN_FP4_CHUNK
                        : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
 }
 
@@ -114,7 +121,10 @@ __host__ __device__ constexpr int chunk_steps() {
 #define ELDR_FFN_MAX_CHUNK 8
 #endif
 // Longest chunk of any pass shape (a chunk's k-steps are unrolled).
-constexpr int kMaxChunk = ELDR_FFN_MAX_CHUNK;
+template <int FMT>
+__host__ __device__ constexpr int max_chunk() {
+  return FMT == kBf16 ? ELDR_FFN_MAX_CHUNK : ELDR_FFN_FP4_MAX_CHUNK;
+}
 __host__ __device__ constexpr int min_c(int a, int b) { return a < b ? a : b; }
 
 // Bytes of one LDS staging buffer (two are used, double-buffered): NT * 16
@@ -129,13 +139,20 @@ enum FfnMode { kUp = 0, kDown = 1 };
 // Waves per workgroup: each wave owns 16 output rows (up: of W1 and of W3)
 // or 32 (down: two 16-row tiles of W2), and all of them share the staged
 // activations.
-template <int MODE>
+#ifndef ELDR_FFN_FP4_UP_WAVES
+#define ELDR_FFN_FP4_UP_WAVES 4
+#endif
+#ifndef ELDR_FFN_FP4_DOWN_WAVES
+#define ELDR_FFN_FP4_DOWN_WAVES 4
+#endif
+template <int MODE, int FMT>
 __host__ __device__ constexpr int ffn_waves() {
-  return MODE == kUp ? ELDR_FFN_UP_WAVES : ELDR_FFN_DOWN_WAVES;
+  return FMT == kBf16 ? (MODE == kUp ? ELDR_FFN_UP_WAVES : ELDR_FFN_DOWN_WAVES)
+                      : (MODE == kUp ? ELDR_FFN_FP4_UP_WAVES : ELDR_FFN_FP4_DOWN_WAVES);
 }
-template <int MODE>
+template <int MODE, int FMT>
 __host__ __device__ constexpr int ffn_threads() {
-  return ffn_waves<MODE>() * kWave;
+  return ffn_waves<MODE, FMT>() * kWave;
 }
 
 struct FfnArgs {
@@ -159,9 +176,9 @@ struct FfnArgs {
 
 // Rows per workgroup: up -> 16 rows per wave (each wave reads the same 16
 // rows of W1 and of W3); down -> 32 rows of W2 per wave (two 16-row tiles).
-template <int MODE>
+template <int MODE, int FMT>
 __host__ __device__ constexpr int rows_per_block() {
-  return MODE == kUp ? ffn_waves<MODE>() * 16 : ffn_waves<MODE>() * 32;
+  return MODE == kUp ? ffn_waves<MODE, FMT>() * 16 : ffn_waves<MODE, FMT>() * 32;
 }
 
 // LDS layout of one staged chunk: per token a row of the chunk's k-steps;
@@ -228,8 +245,8 @@ __device__ __forceinline__ u32x4 expand_fp4(uint32_t w, uint32_t sc) {
 // split, so the down kernel stages h with a plain copy.
 
 template <int MODE, int NT, bool MULTI, int FMT>
-__global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
-  constexpr int kFfnThreads = ffn_threads<MODE>();
+__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs a) {
+  constexpr int kFfnThreads = ffn_threads<MODE, FMT>();
   constexpr int kBuf = lds_buf_bytes<FMT, NT>();
   constexpr int kRing = ring_depth<FMT, NT>();
   constexpr int kSlot = slot_steps<FMT>();  // k-steps per ring slot
@@ -267,13 +284,13 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
   auto run_item = [&](const int e, const int tile, const int s_begin, const int p0, const int c) {
     const int nt = (c + 15) / 16;
 
-    const int r0 = tile * rows_per_block<MODE>() + wave * (MODE == kUp ? 16 : 32);
+    const int r0 = tile * rows_per_block<MODE, FMT>() + wave * (MODE == kUp ? 16 : 32);
     const bool ok0 = r0 < a.rows;
     const bool ok1 = MODE == kUp ? ok0 : (r0 + 16 < a.rows);
     // A 16-row tile past the end of the matrix (only when rows is not a
     // multiple of the band) re-reads the band's first tile and is not stored.
-    const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE>();
-    const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE>());
+    const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE, FMT>();
+    const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE, FMT>());
 
     // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
     // (lane / 16).  Weights are packed (moe_pack_weights): the 64 lane pieces
@@ -305,27 +322,40 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
         rsc[i] = ps[(size_t)si * 16];
       }
     };
-    auto ring_prologue = [&]() {
+    auto ring_prologue = [&](auto N_) {
 #pragma unroll
-      for (int i = 0; i < kRing; ++i) ring_load(i, min(i, nslot - 1));
+      for (int i = 0; i < decltype(N_)::value; ++i) ring_load(i, min(i, nslot - 1));
+    };
+    auto stage_tokens = [&]() {
+      __syncthreads();  // the previous item has finished with LDS
+      if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
+      __syncthreads();
     };
 
-    ring_prologue();
-    __syncthreads();  // the previous item has finished with LDS
-    if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
-    __syncthreads();
+    // bf16 fills the whole ring before the pass shape is chosen; MXFP4's ring
+    // depth depends on the pass shape, so each pass fills its own.
+    if constexpr (FMT == kBf16) {
+      ring_prologue(Int<kRing>{});
+      stage_tokens();
+    }
 
     // Pass shape: NTB token tiles, the LDS buffer split into token rows of
     // kChunk k-steps -- fewer tokens, longer chunks, so every shape fills the
     // same buffer and a small bucket crosses as few barriers as a large one.
     auto run_pass = [&](auto NTB_) {
       constexpr int NTB = decltype(NTB_)::value;
-      constexpr int kChunk = min_c(chunk_steps<FMT, NT>() * NT / NTB, kMaxChunk);
+      constexpr int kChunk = min_c(chunk_steps<FMT, NT>() * NT / NTB, max_chunk<FMT>());
       constexpr int kStride = 128 * kChunk + 16;  // bytes per staged token row: an odd multiple of 16
-      static_assert(kChunk % (kRing * kSlot) == 0, "a chunk is a whole number of ring cycles");
+      // ring slots this pass keeps in flight
+      constexpr int kRingP = FMT == kBf16 ? kRing : min_c(kRing, kChunk / kSlot);
+      static_assert(kChunk % (kRingP * kSlot) == 0, "a chunk is a whole number of ring cycles");
       static_assert(NTB * 16 * kStride <= kBuf, "a chunk fits its buffer");
       constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
       static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
+      if constexpr (FMT == kMxfp4) {
+        ring_prologue(Int<kRingP>{});
+        stage_tokens();
+      }
 
       // Activations are staged in chunks of kChunk k-steps.  Every chunk has
       // the same shape, so the groups a thread moves, their LDS places and the
@@ -384,13 +414,13 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
       }
 
       // One k-step: multiply the weights of chunk-relative step I (ring slot
-      // (I / kSlot) mod kRing) against the staged tokens of step s, and after
-      // a slot's last k-step refill it with the slot kRing ahead.  The refill
+      // (I / kSlot) mod kRingP) against the staged tokens of step s, and after
+      // a slot's last k-step refill it with the slot kRingP ahead.  The refill
       // is issued after the MFMAs that read the slot, into the same
       // registers, and a scheduling barrier keeps it there, so each slot
-      // stays in place and kRing slots of loads are always in flight.
+      // stays in place and kRingP slots of loads are always in flight.
       auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
-        constexpr int i = (decltype(I)::value / kSlot) % kRing;
+        constexpr int i = (decltype(I)::value / kSlot) % kRingP;
         constexpr int j = decltype(I)::value % kSlot;
         const unsigned char* bs = bb + (s - ks) * 128;
         u32x4 a0, a1;
@@ -417,7 +447,7 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
             acc1[t] = mfma16x16x32(a1, bl, acc1[t]);
           }
         }
-        if constexpr (j == kSlot - 1) ring_load(i, min(s / kSlot + kRing, nslot - 1));
+        if constexpr (j == kSlot - 1) ring_load(i, min(s / kSlot + kRingP, nslot - 1));
         __builtin_amdgcn_sched_barrier(0);
       };
 
@@ -426,8 +456,8 @@ __global__ __launch_bounds__(ffn_threads<MODE>()) void ffn_kernel(FfnArgs a) {
       // or itself again), runs kChunk k-steps, unrolled, and publishes the next
       // chunk into the other buffer.  In steady state the staged groups are
       // older than the weight loads behind them, so a publish waits for them
-      // alone.  Chunk starts are multiples of the ring cycle (kRing slots),
-      // so step ks + I sits in ring slot (I / kSlot) % kRing.  The buffer published at the end of iteration ch
+      // alone.  Chunk starts are multiples of the ring cycle (kRingP slots),
+      // so step ks + I sits in ring slot (I / kSlot) % kRingP.  The buffer published at the end of iteration ch
       // was last read in iteration ch - 1, before the previous barrier.
       const int nfull = nk / kChunk;
       const int last_start = ((nk - 1) / kChunk) * kChunk;
@@ -566,13 +596,13 @@ static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
   if (T <= NT * 16) {
     a.extra_groups = 0;
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, false, FMT>), dim3(kNumXcd * a.tiles * per_xcd),
-                       dim3(ffn_threads<MODE>()), 0, s, a);
+                       dim3(ffn_threads<MODE, FMT>()), 0, s, a);
   } else {
     const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
     a.extra_groups = extra;
     a.max_groups = (T + NT * 16 - 1) / (NT * 16);
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, true, FMT>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
-                       dim3(ffn_threads<MODE>()), 0, s, a);
+                       dim3(ffn_threads<MODE, FMT>()), 0, s, a);
   }
 }
 
@@ -629,7 +659,8 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint1
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w1, w3, offsets, perm_token, union_ids,
                    union_size, ws, d.I, d.H, 0, 0, 1, d.E, nullptr, nullptr};
-  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
+  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp, eldr::kBf16>() - 1) /
+             eldr::rows_per_block<eldr::kUp, eldr::kBf16>();
   eldr::launch_ffn_nt<eldr::kUp, eldr::kBf16>(up, d.T, d.K, d.E, s);
   return launch_status();
 }
@@ -650,7 +681,8 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, nullptr, offsets, perm_token,
                      union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E, nullptr, nullptr};
   down.tiles =
-      (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
+      (d.H + eldr::rows_per_block<eldr::kDown, eldr::kBf16>() - 1) /
+      eldr::rows_per_block<eldr::kDown, eldr::kBf16>();
   eldr::launch_ffn_nt<eldr::kDown, eldr::kBf16>(down, d.T, d.K, d.E,
                                                reinterpret_cast<hipStream_t>(stream));
   return launch_status();
@@ -713,7 +745,8 @@ extern "C" int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes,
                    union_ids, union_size, ws, d.I, d.H, 0, 0, 1, d.E,
                    reinterpret_cast<const eldr::u32x4*>(up_codes),
                    reinterpret_cast<const uint32_t*>(up_scales)};
-  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp>() - 1) / eldr::rows_per_block<eldr::kUp>();
+  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp, eldr::kMxfp4>() - 1) /
+             eldr::rows_per_block<eldr::kUp, eldr::kMxfp4>();
   eldr::launch_ffn_nt<eldr::kUp, eldr::kMxfp4>(up, d.T, d.K, d.E,
                                               reinterpret_cast<hipStream_t>(stream));
   return launch_status();
@@ -739,7 +772,8 @@ extern "C" int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_cod
                      reinterpret_cast<const eldr::u32x4*>(down_codes),
                      reinterpret_cast<const uint32_t*>(down_scales)};
   down.tiles =
-      (d.H + eldr::rows_per_block<eldr::kDown>() - 1) / eldr::rows_per_block<eldr::kDown>();
+      (d.H + eldr::rows_per_block<eldr::kDown, eldr::kMxfp4>() - 1) /
+      eldr::rows_per_block<eldr::kDown, eldr::kMxfp4>();
   eldr::launch_ffn_nt<eldr::kDown, eldr::kMxfp4>(down, d.T, d.K, d.E,
                                                 reinterpret_cast<hipStream_t>(stream));
   return launch_status();
