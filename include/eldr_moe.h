@@ -232,8 +232,8 @@ int moe_pack_mxfp4_down(const uint8_t* w2_codes, const uint8_t* w2_scales, int32
  * registers (exact: an E2M1 value times a power of two in range is a bf16
  * number) and multiplied exactly as in moe_expert_ffn, so the result equals
  * moe_expert_ffn's on the dequantized weights.  Each active expert's codes
- * and scales are streamed once per call when it has at most 32 tokens; a
- * bigger bucket is split into groups of 32 tokens sharing the XCD's L2.
+ * and scales are streamed once per call when it has at most 64 tokens; a
+ * bigger bucket is split into groups of 64 tokens sharing the XCD's L2.
  * Other arguments, the workspace (moe_ffn_workspace_bytes) and the error
  * behaviour are those of moe_expert_ffn; in addition H % 64 == 0 and
  * I % 64 == 0 (else MOE_ERR_UNSUPPORTED), and the scale pointers must be

@@ -85,12 +85,14 @@ __host__ __device__ constexpr int slot_steps() {
   return FMT == kBf16 ? 1 : 2;
 }
 
-// Token tiles of 16 per item: at most 64 tokens of an expert for bf16, 32
-// for MXFP4 (whose MFMA and LDS work per weight byte is four times bf16's; a
-// larger bucket takes more token groups, served from L2).
+// Token tiles of 16 per item: at most 64 tokens of an expert (a larger bucket
+// takes more token groups, served from L2).
 template <int FMT>
 __host__ __device__ constexpr int max_tiles() {
-  return FMT == kBf16 ? 4 : 2;
+#ifndef ELDR_FFN_FP4_MAX_TILES
+#define ELDR_FFN_FP4_MAX_TILES 4
+#endif
+  return FMT == kBf16 ? 4 : ELDR_FFN_FP4_MAX_TILES;
 }
 
 // Ring slots of weights in flight per wave (the prefetch depth of the ring;
@@ -110,11 +112,16 @@ __host__ __device__ constexpr int ring_depth() {
 #define ELDR_FFN_CYCLES2 1
 #endif
 // MXFP4 moves a quarter of bf16's bytes per k-step, so it needs longer
-// chunks for the same bytes in flight: 16 token rows of 16 k-steps, or 32 of 8.
+// chunks for the same bytes in flight, in the same 33 KB buffer: 16 token
+// rows of 16 k-steps, 32 of 8, or 64 of 4 (a pass with fewer tiles than its
+// kernel lengthens its chunks, up to 16 k-steps).
 template <int FMT, int NT>
 __host__ __device__ constexpr int chunk_steps() {
-  return FMT == kMxfp4 ? (NT == 1 ? 2 : 1) * ELDR_FFN_FP4_CHUNK
-                       : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
+  return FMT == kMxfp4
+             ? (NT == 1   ? 2 * ELDR_FFN_FP4_CHUNK
+                : NT == 2 ? ELDR_FFN_FP4_CHUNK
+                          : ELDR_FFN_FP4_CHUNK / 2)
+             : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
 }
 
 #ifndef ELDR_FFN_MAX_CHUNK
@@ -457,8 +464,9 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
       // chunk into the other buffer.  In steady state the staged groups are
       // older than the weight loads behind them, so a publish waits for them
       // alone.  Chunk starts are multiples of the ring cycle (kRingP slots),
-      // so step ks + I sits in ring slot (I / kSlot) % kRingP.  The buffer published at the end of iteration ch
-      // was last read in iteration ch - 1, before the previous barrier.
+      // so step ks + I sits in ring slot (I / kSlot) % kRingP.  The buffer
+      // published at the end of iteration ch was last read in iteration
+      // ch - 1, before the previous barrier.
       const int nfull = nk / kChunk;
       const int last_start = ((nk - 1) / kChunk) * kChunk;
       fetch(0);
