@@ -21,8 +21,9 @@ extern "C" {
 /*
  * moe_stream_read_probe -- read `bytes` bytes at `buf` (device memory,
  * 16-byte aligned, bytes a multiple of 16) exactly once: 2048 workgroups of
- * 256 threads, each workgroup a contiguous stretch, 16-byte loads with eight
- * per thread in flight.  The loaded words are folded into a checksum that is
+ * 256 threads, each workgroup a contiguous stretch, non-temporal 16-byte
+ * loads (the hint the expert FFN's weight loads carry) with eight per thread
+ * in flight.  The loaded words are folded into a checksum that is
  * stored to sink[0] (one uint32 on the device) only if it equals a fixed
  * constant, so the loads cannot be optimised away and nothing else is
  * written.  Asynchronous on `stream`; returns MOE_OK or a negative code.

@@ -391,6 +391,16 @@ class LayerBuffers:
         )
 
 
+def _gate_and_bucket(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream) -> None:
+    if routing is None:
+        moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
+    else:
+        buf.topk_ids.copy_(routing[0])
+        buf.topk_w.copy_(routing[1])
+    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
+               buf.union_ids, buf.union_size, stream)
+
+
 def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
     """One decode-step MoE layer: the four calls back to back on one stream.
 
@@ -399,13 +409,7 @@ def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None
     ``routing=(topk_ids, topk_w)`` bypasses the gate (the ids are copied into
     ``buf``).  Returns ``buf.out``.
     """
-    if routing is None:
-        moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
-    else:
-        buf.topk_ids.copy_(routing[0])
-        buf.topk_w.copy_(routing[1])
-    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
-               buf.union_ids, buf.union_size, stream)
+    _gate_and_bucket(x, w_gate, d, buf, routing, stream)
     moe_expert_ffn(x, w1, w3, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
                    buf.y_perm, buf.ws, stream)
     moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
@@ -414,13 +418,7 @@ def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None
 
 def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
     """moe_layer with MXFP4 experts: ``up`` and ``down`` from pack_mxfp4_expert_weights."""
-    if routing is None:
-        moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
-    else:
-        buf.topk_ids.copy_(routing[0])
-        buf.topk_w.copy_(routing[1])
-    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
-               buf.union_ids, buf.union_size, stream)
+    _gate_and_bucket(x, w_gate, d, buf, routing, stream)
     moe_expert_ffn_mxfp4(x, up, down, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
                          d, buf.y_perm, buf.ws, stream)
     moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
