@@ -10,7 +10,11 @@
 
 namespace eldr {
 
-constexpr int kGateWaves = 4;        // the reduction axis H is split over the 4 waves
+#ifndef ELDR_GATE_WAVES
+#define ELDR_GATE_WAVES 8
+#endif
+constexpr int kGateWaves = ELDR_GATE_WAVES;  // the reduction axis H is split over the waves
+constexpr int kGateThreads = kGateWaves * 64;
 constexpr int kGateExperts = 4;      // experts per workgroup
 constexpr int kGateTokens = 8;       // tokens per workgroup
 constexpr int kGateOut = kGateExperts * kGateTokens;  // 32 sums per workgroup
@@ -28,13 +32,15 @@ __device__ __forceinline__ void halving_step(float* acc, int lane) {
   }
 }
 
-// A workgroup scores 4 experts for 8 tokens.  Wave w covers the w-th quarter
-// of H; lane l accumulates, for all 32 (expert, token) pairs, the products at
-// float4 positions q = l, l + 64, ... of that quarter, in the same order for
-// every expert.  The 64 lane partials are summed by a halving butterfly and
-// the 4 wave partials in wave order, so the reduction tree does not depend on
-// the expert: experts with identical gate rows get bitwise-identical scores.
-__global__ __launch_bounds__(256) void gate_scores_kernel(const float* __restrict__ x,
+// A workgroup scores 4 experts for 8 tokens.  Wave w covers the w-th of
+// kGateWaves slices of H; lane l accumulates, for all 32 (expert, token)
+// pairs, the products at float4 positions q = l, l + 64, ... of that slice,
+// in the same order for every expert.  The 64 lane partials are summed by a
+// halving butterfly and the wave partials in wave order, so the reduction
+// tree does not depend on the expert: experts with identical gate rows get
+// bitwise-identical scores.  With 8 waves a lane takes one float4 of each
+// row at H = 2048, so the loads cost a single memory round trip.
+__global__ __launch_bounds__(kGateThreads) void gate_scores_kernel(const float* __restrict__ x,
                                                           const float* __restrict__ wg, int T,
                                                           int H, int E,
                                                           float* __restrict__ logits) {
@@ -104,7 +110,9 @@ __global__ __launch_bounds__(256) void gate_scores_kernel(const float* __restric
     const int o = threadIdx.x;
     const int a = o / kGateTokens;
     const int j = o % kGateTokens;
-    const float v = ((part[0][o] + part[1][o]) + part[2][o]) + part[3][o];
+    float v = part[0][o];
+#pragma unroll
+    for (int w = 1; w < kGateWaves; ++w) v += part[w][o];
     if (e0 + a < E && t0 + j < T) logits[(size_t)(t0 + j) * E + e0 + a] = v;
   }
 }
@@ -112,47 +120,53 @@ __global__ __launch_bounds__(256) void gate_scores_kernel(const float* __restric
 // Selection by rank.  Thread (t, e) counts the experts that precede e in the
 // selection order of token t (a larger logit, or an equal logit and a lower
 // id); e is selected iff that rank is below K, and the rank is its position
-// in topk_ids.  Every comparison is exact, so the result is the oracle's
-// order whatever the thread schedule.  Rows are staged in LDS padded with
-// -inf to a multiple of 4 (-inf precedes nothing).  The K picks then form
-// the softmax over themselves, summed in rank order.
+// in topk_ids.  The order is folded into one 64-bit key per expert -- the
+// logit's bits mapped to an unsigned integer of the same order (with -0 taken
+// as +0, so equal logits get equal high words), then the complement of the
+// id -- so that "precedes" is a single unsigned comparison of keys, and keys
+// are distinct.  Every comparison is exact, so the result is the oracle's
+// order whatever the thread schedule.  Rows of keys are staged in LDS, padded
+// with 0 (below every key) to an even length.  The K picks then form the
+// softmax over themselves, summed in rank order.
 constexpr int kSelectThreads = 256;
+
+__device__ __forceinline__ uint64_t select_key(float v, int e) {
+  uint32_t b = __float_as_uint(v + 0.0f);  // -0 -> +0
+  b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)b << 32) | (uint32_t)~(uint32_t)e;
+}
+
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 
 __global__ __launch_bounds__(kSelectThreads) void gate_select_kernel(
     const float* __restrict__ logits, int T, int E, int K, int tokens_per_block,
     int32_t* __restrict__ ids, float* __restrict__ wts) {
-  extern __shared__ float sl[];                 // [tokens_per_block][Ep] logits, -inf padded
-  const int Ep = (E + 3) & ~3;
-  float* sel = sl + tokens_per_block * Ep;      // [tokens_per_block][MOE_MAX_K] exp(l - lmax)
+  extern __shared__ uint64_t skey[];            // [tokens_per_block][Ep] keys, 0 padded
+  const int Ep = (E + 1) & ~1;
+  float* sel = reinterpret_cast<float*>(skey + tokens_per_block * Ep);  // [tpb][MOE_MAX_K] exp
   __shared__ float lmax[kSelectThreads];
   const int t0 = blockIdx.x * tokens_per_block;
   const int nt = min(tokens_per_block, T - t0);
-  for (int i = threadIdx.x; i < nt * Ep; i += kSelectThreads) {
-    const int t = i / Ep;
-    const int e = i - t * Ep;
-    sl[i] = e < E ? logits[(size_t)(t0 + t) * E + e] : -INFINITY;
-  }
-  __syncthreads();
   const int p = threadIdx.x;  // one (token, expert) pair per thread
   const bool live = p < nt * E;
   const int t = live ? p / E : 0;
   const int e = p - t * E;
+  const float v = live ? logits[(size_t)(t0 + t) * E + e] : 0.0f;
+  const uint64_t mine = select_key(v, e);
+  if (live) skey[t * Ep + e] = mine;
+  if (p < nt && (E & 1)) skey[p * Ep + E] = 0;
+  __syncthreads();
   int rank = K;
-  float v = 0.0f;
   if (live) {
-    const float4* row = reinterpret_cast<const float4*>(sl + t * Ep);
-    v = sl[t * Ep + e];
-    int r = 0;
+    const u64x2* row = reinterpret_cast<const u64x2*>(skey + t * Ep);
+    int r0 = 0, r1 = 0;
 #pragma unroll 8
-    for (int f4 = 0; f4 < Ep / 4; ++f4) {
-      const float4 u = row[f4];
-      const int f = 4 * f4;
-      r += (u.x > v || (u.x == v && f + 0 < e)) ? 1 : 0;
-      r += (u.y > v || (u.y == v && f + 1 < e)) ? 1 : 0;
-      r += (u.z > v || (u.z == v && f + 2 < e)) ? 1 : 0;
-      r += (u.w > v || (u.w == v && f + 3 < e)) ? 1 : 0;
+    for (int f2 = 0; f2 < Ep / 2; ++f2) {
+      const u64x2 k = row[f2];
+      r0 += k.x > mine ? 1 : 0;
+      r1 += k.y > mine ? 1 : 0;
     }
-    rank = r;
+    rank = r0 + r1;
     if (rank == 0) lmax[t] = v;  // rank 0 holds the largest logit
   }
   __syncthreads();
@@ -185,14 +199,14 @@ extern "C" int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, fl
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   dim3 g1((d.E + eldr::kGateExperts - 1) / eldr::kGateExperts,
           (d.T + eldr::kGateTokens - 1) / eldr::kGateTokens);
-  hipLaunchKernelGGL(eldr::gate_scores_kernel, g1, dim3(256), 0, s, x, w_gate, d.T, d.H, d.E,
+  hipLaunchKernelGGL(eldr::gate_scores_kernel, g1, dim3(eldr::kGateThreads), 0, s, x, w_gate, d.T, d.H, d.E,
                      logits);
   st = launch_status();
   if (st != MOE_OK) return st;
   // As many tokens per workgroup as give every thread one (token, expert)
   // pair (E <= 256, so at least one token).
   const int tpb = eldr::kSelectThreads / d.E;
-  const size_t lds = (size_t)tpb * (((d.E + 3) & ~3) + MOE_MAX_K) * sizeof(float);
+  const size_t lds = (size_t)tpb * (((d.E + 1) & ~1) * sizeof(uint64_t) + MOE_MAX_K * sizeof(float));
   dim3 g2((d.T + tpb - 1) / tpb);
   hipLaunchKernelGGL(eldr::gate_select_kernel, g2, dim3(eldr::kSelectThreads), lds, s, logits, d.T,
                      d.E, d.K, tpb, topk_ids, topk_w);
