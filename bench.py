@@ -119,7 +119,7 @@ class Bench:
             self.weights.append(tuple(w.clone() for w in self.weights[0]))
 
     def step(self, i: int, routing=None, ev=None) -> None:
-        w1, w3, w2 = self.weights[i % len(self.weights)]
+        w13, w2 = self.weights[i % len(self.weights)]
         d, b = self.d, self.buf
         if routing is None:
             B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
@@ -130,8 +130,7 @@ class Bench:
                      b.union_size)
         if ev is not None:
             ev[0].record(self.stream)
-        B.moe_expert_ffn_up(self.x, w1, w3, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
-                            b.ws)
+        B.moe_expert_ffn_up(self.x, w13, b.offsets, b.perm_token, b.union_ids, b.union_size, d, b.ws)
         if ev is not None:
             ev[1].record(self.stream)
         B.moe_expert_ffn_down(b.ws, w2, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
@@ -466,9 +465,9 @@ class MultiLayer:
     def step(self, routing=None) -> None:
         """One decode step; routing[l] = (ids, w) device tensors, or None for the gate."""
         for l in range(self.n_layers):
-            x, wg, (w1, w3, w2) = self.layers[l % len(self.layers)]
+            x, wg, (w13, w2) = self.layers[l % len(self.layers)]
             r = None if routing is None else routing[l]
-            B.moe_layer(x, wg, w1, w3, w2, self.d, self.bufs[l], routing=r)
+            B.moe_layer(x, wg, w13, w2, self.d, self.bufs[l], routing=r)
 
     def unions(self) -> list[int]:
         torch.cuda.synchronize()
@@ -737,8 +736,8 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
 
             def run():
                 for layer in range(layers_timed):
-                    w1, w3, w2 = packed[layer % 2]
-                    B.moe_layer(x, wg, w1, w3, w2, d, buf, routing=routes[layer])
+                    w13, w2 = packed[layer % 2]
+                    B.moe_layer(x, wg, w13, w2, d, buf, routing=routes[layer])
 
             side = torch.cuda.Stream()
             side.wait_stream(torch.cuda.current_stream())

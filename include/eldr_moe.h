@@ -32,8 +32,9 @@
  *   contiguous along the reduction axis):
  *     w_gate [E, H] fp32; w1, w3 [E, I, H] bf16; w2 [E, H, I] bf16.
  *   The math is y = W2 (silu(W1 x) * (W3 x)) with silu(z) = z / (1 + e^-z).
- *   The expert FFN takes w1, w3 and w2 *packed* by moe_pack_weights (a
- *   permutation done once, when the model is loaded; see below).
+ *   The expert FFN takes the expert weights *packed* by moe_pack_up_weights
+ *   (w1 with w3) and moe_pack_down_weights (w2), a permutation done once,
+ *   when the model is loaded (see below).
  * - Pointers to fp32 or bf16 arrays must be 16-byte aligned (the kernels use
  *   128-bit loads and stores); int32 arrays 4-byte aligned.
  * - T = 0 (an empty batch) is accepted everywhere: nothing is computed except
@@ -118,20 +119,33 @@ int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* of
                int32_t* union_size, void* stream);
 
 /*
- * moe_pack_weights -- permute one expert weight tensor [E, R, K] (bf16,
- * row-major [out, in]) into the fragment layout the expert FFN streams.
- * Output element order: for each expert e, 16-row band b (R / 16 of them),
- * k-step s (K / 32 of them) and lane l (0..63), the 8 values
- *   src[e, 16 b + (l % 16), 32 s + 8 (l / 16) + j], j = 0..7,
- * i.e. one 16 x 32 MFMA A fragment per 1 KB, lanes in order, so that each
- * load of the FFN reads 1 KB of consecutive memory.  Values and size are
- * unchanged (E * R * K bf16).  Call once per tensor, off the decode path:
- * w1 and w3 with (R, K) = (I, H), w2 with (R, K) = (H, I).
- * src and dst are distinct 16-byte-aligned device buffers; R % 16 == 0 and
- * K % 32 == 0.  Asynchronous on `stream`.
+ * moe_pack_up_weights / moe_pack_down_weights -- lay the bf16 expert weights
+ * out as the expert FFN streams them.  Call once per layer, off the decode
+ * path (when the model is loaded); asynchronous on `stream`.
+ *
+ * The FFN reads 16-row x 32-column tiles as MFMA A fragments: lane l
+ * (0..63) takes row l % 16 and the 8 values starting at column 8 (l / 16).
+ * One fragment is 1 KB, its 64 lane pieces in lane order.  A workgroup item
+ * is a band of rows -- up: 64 rows of W1 and the same 64 rows of W3; down:
+ * 128 rows of W2 -- handled by 4 waves, each reading two fragments per
+ * k-step of 32 values: up wave w: rows 16 w .. 16 w + 15 of the band, of W1
+ * then W3; down wave w: rows 32 w .. 32 w + 15, then 32 w + 16 .. 32 w + 31.
+ * The packed order is, for each expert, band, k-step, wave (w ascending)
+ * and its two fragments, the fragment's 64 lane pieces, so that one item is
+ * one contiguous stretch of memory.  A last band with fewer rows (R not a
+ * multiple of the band) holds only its waves' fragments.
+ *
+ *   moe_pack_up_weights:   w1, w3 [E, I, H] -> w13, 2 * E * I * H bf16
+ *   moe_pack_down_weights: w2 [E, H, I]     -> w2p, E * H * I bf16
+ *
+ * Values are unchanged (a permutation).  Inputs and output are distinct
+ * 16-byte-aligned device buffers; I % 32 == 0 and H % 32 == 0 (else
+ * MOE_ERR_UNSUPPORTED).
  */
-int moe_pack_weights(const uint16_t* src, int32_t E, int32_t R, int32_t K, uint16_t* dst,
-                     void* stream);
+int moe_pack_up_weights(const uint16_t* w1, const uint16_t* w3, int32_t E, int32_t I, int32_t H,
+                        uint16_t* w13, void* stream);
+int moe_pack_down_weights(const uint16_t* w2, int32_t E, int32_t H, int32_t I, uint16_t* w2p,
+                          void* stream);
 
 /* Bytes of device workspace moe_expert_ffn needs for dims d: the SwiGLU
  * activations of every slot, stored as pairs of bf16 values (4 bytes a
@@ -153,8 +167,9 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * The grid is sized from E and T alone and reads union_size on the device,
  * so no host synchronisation is needed between moe_bucket and this call.
  *
- * x [T, H] fp32; w1, w3 ([E, I, H]) and w2 ([E, H, I]) bf16 packed by
- * moe_pack_weights; offsets [E+1],
+ * x [T, H] fp32; w13 (W1 and W3, [E, I, H] each) packed by
+ * moe_pack_up_weights and w2 ([E, H, I]) packed by moe_pack_down_weights;
+ * offsets [E+1],
  * perm_token [T*K], union_ids [E], union_size [1] int32 (moe_bucket output).
  * y_perm [T*K, H] fp32 output (rows of slots whose expert is not in the
  * union are not written).  ws: device workspace of at least
@@ -163,7 +178,7 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * values (high part and rounded remainder, about 16 significant bits) on
  * MFMA with fp32 accumulation.
  */
-int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+int moe_expert_ffn(const float* x, const uint16_t* w13, const uint16_t* w2,
                    const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,
                    const int32_t* union_size, moe_dims d, float* y_perm, void* ws,
                    size_t ws_bytes, void* stream);
@@ -180,8 +195,8 @@ int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t* w3, const
  * moe_expert_ffn; ws_bytes is the size of the workspace `ws`, which must be
  * the one the preceding moe_expert_ffn_up call filled.
  */
-int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint16_t* w3,
-                      const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,
+int moe_expert_ffn_up(const float* x, const uint16_t* w13, const int32_t* offsets,
+                      const int32_t* perm_token, const int32_t* union_ids,
                       const int32_t* union_size, moe_dims d, void* ws, size_t ws_bytes,
                       void* stream);
 int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offsets,

@@ -51,15 +51,13 @@ _SIGNATURES = {
     "moe_gate_topk": (ctypes.c_int, [_vp, _vp, MoeDims, _vp, _vp, _vp, _vp]),
     "moe_bucket": (ctypes.c_int, [_vp, MoeDims, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "moe_ffn_workspace_bytes": (ctypes.c_size_t, [MoeDims]),
-    "moe_expert_ffn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, MoeDims, _vp, _vp,
-                                      ctypes.c_size_t, _vp]),
-    "moe_expert_ffn_up": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, MoeDims, _vp,
-                                         ctypes.c_size_t, _vp]),
+    "moe_expert_ffn": (ctypes.c_int, [_vp] * 7 + [MoeDims, _vp, _vp, ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_up": (ctypes.c_int, [_vp] * 6 + [MoeDims, _vp, ctypes.c_size_t, _vp]),
     "moe_expert_ffn_down": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, MoeDims, ctypes.c_size_t,
                                            _vp, _vp]),
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
-    "moe_pack_weights": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
-                                        _vp]),
+    "moe_pack_up_weights": (ctypes.c_int, [_vp, _vp] + [ctypes.c_int32] * 3 + [_vp, _vp]),
+    "moe_pack_down_weights": (ctypes.c_int, [_vp] + [ctypes.c_int32] * 3 + [_vp, _vp]),
     "moe_pack_mxfp4_up": (ctypes.c_int, [_vp, _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_int32, _vp, _vp, _vp]),
     "moe_pack_mxfp4_down": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -178,22 +176,20 @@ def moe_ffn_workspace_bytes(d: MoeDims) -> int:
     return int(load().moe_ffn_workspace_bytes(d))
 
 
-def moe_expert_ffn(x, w1, w3, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
+def moe_expert_ffn(x, w13, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
                    ws, stream=None) -> None:
+    """The expert FFN of the union; w13 and w2 as packed by ``pack_expert_weights``."""
     _need(x, "x", torch.float32, d.T * d.H)
-    for name, w, n in (("w1", w1, d.E * d.I * d.H), ("w3", w3, d.E * d.I * d.H),
-                       ("w2", w2, d.E * d.H * d.I)):
-        _need(w, name, torch.bfloat16, n)
+    _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
+    _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
     _need(offsets, "offsets", torch.int32, d.E + 1)
     _need(perm_token, "perm_token", torch.int32, d.T * d.K)
     _need(union_ids, "union_ids", torch.int32, d.E)
     _need(union_size, "union_size", torch.int32, 1)
     _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
-    if ws.device.type != "cuda" or not ws.is_contiguous():
-        raise ValueError("ws: must be a contiguous device tensor")
-    ws_bytes = ws.numel() * ws.element_size()
+    ws_bytes = _need_ws(ws, d)
     _check("moe_expert_ffn", load().moe_expert_ffn(
-        _ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(x), _ptr(w13), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
         _ptr(union_size), d, _ptr(y_perm), _ptr(ws), ws_bytes, _stream(stream)))
 
 
@@ -203,14 +199,13 @@ def _need_ws(ws, d: MoeDims) -> int:
     return ws.numel() * ws.element_size()
 
 
-def moe_expert_ffn_up(x, w1, w3, offsets, perm_token, union_ids, union_size, d: MoeDims, ws,
+def moe_expert_ffn_up(x, w13, offsets, perm_token, union_ids, union_size, d: MoeDims, ws,
                       stream=None) -> None:
     _need(x, "x", torch.float32, d.T * d.H)
-    _need(w1, "w1", torch.bfloat16, d.E * d.I * d.H)
-    _need(w3, "w3", torch.bfloat16, d.E * d.I * d.H)
+    _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
     ws_bytes = _need_ws(ws, d)
     _check("moe_expert_ffn_up", load().moe_expert_ffn_up(
-        _ptr(x), _ptr(w1), _ptr(w3), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(x), _ptr(w13), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
         _ptr(union_size), d, _ptr(ws), ws_bytes, _stream(stream)))
 
 
@@ -224,22 +219,38 @@ def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: M
         ws_bytes, _ptr(y_perm), _stream(stream)))
 
 
-def moe_pack_weights(src, dst=None, stream=None) -> torch.Tensor:
-    """Pack one expert weight tensor [E, R, K] (bf16) for the expert FFN; returns dst."""
-    if src.dim() != 3:
-        raise ValueError("src: expected [E, R, K]")
-    E, R, K = (int(v) for v in src.shape)
-    _need(src, "src", torch.bfloat16, E * R * K)
+def moe_pack_up_weights(w1, w3, dst=None, stream=None) -> torch.Tensor:
+    """Pack W1 and W3 ([E, I, H] bf16 each) into one band-interleaved tensor; returns dst."""
+    if w1.dim() != 3 or w1.shape != w3.shape:
+        raise ValueError("w1, w3: expected two [E, I, H] tensors")
+    E, I, H = (int(v) for v in w1.shape)
+    _need(w1, "w1", torch.bfloat16, E * I * H)
+    _need(w3, "w3", torch.bfloat16, E * I * H)
     if dst is None:
-        dst = torch.empty_like(src)
-    _need(dst, "dst", torch.bfloat16, E * R * K)
-    _check("moe_pack_weights", load().moe_pack_weights(_ptr(src), E, R, K, _ptr(dst), _stream(stream)))
+        dst = torch.empty((E, 2 * I, H), dtype=torch.bfloat16, device=w1.device)
+    _need(dst, "dst", torch.bfloat16, 2 * E * I * H)
+    _check("moe_pack_up_weights", load().moe_pack_up_weights(_ptr(w1), _ptr(w3), E, I, H, _ptr(dst),
+                                                             _stream(stream)))
+    return dst
+
+
+def moe_pack_down_weights(w2, dst=None, stream=None) -> torch.Tensor:
+    """Pack W2 ([E, H, I] bf16) band by band for the down projection; returns dst."""
+    if w2.dim() != 3:
+        raise ValueError("w2: expected [E, H, I]")
+    E, H, I = (int(v) for v in w2.shape)
+    _need(w2, "w2", torch.bfloat16, E * H * I)
+    if dst is None:
+        dst = torch.empty_like(w2)
+    _need(dst, "dst", torch.bfloat16, E * H * I)
+    _check("moe_pack_down_weights", load().moe_pack_down_weights(_ptr(w2), E, H, I, _ptr(dst),
+                                                                 _stream(stream)))
     return dst
 
 
 def pack_expert_weights(w1, w3, w2, stream=None):
-    """Pack (w1 [E,I,H], w3 [E,I,H], w2 [E,H,I]) for moe_expert_ffn."""
-    return tuple(moe_pack_weights(w, stream=stream) for w in (w1, w3, w2))
+    """Pack (w1 [E,I,H], w3 [E,I,H], w2 [E,H,I]) for moe_expert_ffn: returns (w13, w2p)."""
+    return (moe_pack_up_weights(w1, w3, stream=stream), moe_pack_down_weights(w2, stream=stream))
 
 
 # ----------------------------------------------------------------------------- MXFP4 experts
@@ -401,16 +412,16 @@ def _gate_and_bucket(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream) 
                buf.union_ids, buf.union_size, stream)
 
 
-def moe_layer(x, w_gate, w1, w3, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
+def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
     """One decode-step MoE layer: the four calls back to back on one stream.
 
-    w1, w3 and w2 are the expert weights packed by ``pack_expert_weights``.
+    w13 and w2 are the expert weights packed by ``pack_expert_weights``.
 
     ``routing=(topk_ids, topk_w)`` bypasses the gate (the ids are copied into
     ``buf``).  Returns ``buf.out``.
     """
     _gate_and_bucket(x, w_gate, d, buf, routing, stream)
-    moe_expert_ffn(x, w1, w3, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
+    moe_expert_ffn(x, w13, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
                    buf.y_perm, buf.ws, stream)
     moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
     return buf.out

@@ -10,8 +10,10 @@
 //   Within each launch a workgroup item is one expert, one band of output
 //   rows and up to 64 of the expert's tokens; it streams the band's bf16
 //   weights from HBM (128-bit loads straight into the MFMA A operand).
-//   Weights come packed by moe_pack_weights, so each load instruction reads
-//   one contiguous 1 KB MFMA fragment.
+//   Weights come packed by band (moe_pack_up_weights, moe_pack_down_weights):
+//   each load instruction reads one contiguous 1 KB MFMA fragment, and a
+//   workgroup's loads of one k-step are adjacent, so an item is one
+//   contiguous stream.
 // * An expert with at most 64 tokens has one item per band, so its weights
 //   are read once.  A bigger bucket is split into token groups of 64 whose
 //   items for one band get adjacent workgroup slots on one XCD: they run side
@@ -69,8 +71,9 @@ constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fr
 constexpr int kMaxExpertsPerXcd = (MOE_MAX_E + kNumXcd - 1) / kNumXcd;
 
 // Weight formats.
-//   kBf16:  packed by moe_pack_weights; a ring slot is one k-step of the
-//           wave's two 16-row tiles, two 1 KB loads.
+//   kBf16:  packed by moe_pack_up_weights / moe_pack_down_weights; a ring
+//           slot is one k-step of the wave's two 16-row tiles, two adjacent
+//           1 KB loads.
 //   kMxfp4: packed by moe_pack_mxfp4_up / _down; a ring slot is two k-steps
 //           of the wave's two 16-row tiles: one 1 KB load of FP4 codes (a
 //           lane's 16 bytes are its 8 codes of tile 0 step 0, tile 0 step 1,
@@ -164,8 +167,7 @@ __host__ __device__ constexpr int ffn_threads() {
 
 struct FfnArgs {
   const uint4* src;            // up: x [T, H] fp32; down: h [T*K, I] as bf16 pairs
-  const uint16_t* wa;          // up: W1 [E, I, H]; down: W2 [E, H, I]
-  const uint16_t* wb;          // up: W3 [E, I, H]; down: unused
+  const uint16_t* wa;          // bf16, packed by band: up W1 and W3; down W2
   const int32_t* offsets;      // [E+1]
   const int32_t* perm_token;   // [T*K]
   const int32_t* union_ids;    // [E]
@@ -284,7 +286,6 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
   const int nslot = nk / kSlot;  // ring slots of a row band
   const int arow = lane & 15;
   const int kgrp = lane >> 4;
-  const size_t tiles_per_expert = (size_t)(a.rows / 16);
 
   // One item: the token group of up to kGroupTokens tokens starting at slot
   // s_begin + p0 of expert e's bucket, against row band `tile`.
@@ -294,19 +295,28 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     const int r0 = tile * rows_per_block<MODE, FMT>() + wave * (MODE == kUp ? 16 : 32);
     const bool ok0 = r0 < a.rows;
     const bool ok1 = MODE == kUp ? ok0 : (r0 + 16 < a.rows);
-    // A 16-row tile past the end of the matrix (only when rows is not a
-    // multiple of the band) re-reads the band's first tile and is not stored.
+    // MXFP4: a 16-row tile past the end of the matrix (only when rows is not
+    // a multiple of the band) re-reads the band's first tile and is not stored.
     const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE, FMT>();
-    const int ra1 = MODE == kUp ? ra0 : (ok1 ? r0 + 16 : tile * rows_per_block<MODE, FMT>());
 
     // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
-    // (lane / 16).  Weights are packed (moe_pack_weights): the 64 lane pieces
-    // of one tile and k-step are a contiguous 1 KB fragment, and a tile's
-    // k-steps follow each other, so step s of a tile is at tile_base + s * 512.
-    const uint16_t* pa0 =
-        a.wa + ((e * tiles_per_expert + ra0 / 16) * nk) * kFragElems + lane * 8;
-    const uint16_t* pa1 = (MODE == kUp ? a.wb : a.wa) +
-                          ((e * tiles_per_expert + ra1 / 16) * nk) * kFragElems + lane * 8;
+    // (lane / 16).  bf16 weights are packed by band (moe_pack_up_weights,
+    // moe_pack_down_weights): for each k-step the band's waves' two 1 KB
+    // fragments lie side by side (up: W1 then W3 of the wave's 16 rows; down:
+    // the wave's two 16-row tiles of W2), so the workgroup streams one
+    // contiguous stretch.  A wave past a short last band re-reads the band's
+    // last wave and stores nothing.
+    constexpr int kWaveRows = MODE == kUp ? 16 : 32;
+    constexpr int kMats = MODE == kUp ? 2 : 1;  // matrices a band interleaves
+    const int waves_b = min(rows_per_block<MODE, FMT>(), a.rows - tile * rows_per_block<MODE, FMT>()) /
+                        kWaveRows;
+    const int wc = min(wave, waves_b - 1);
+    const size_t step_elems = (size_t)waves_b * 2 * kFragElems;
+    const uint16_t* pa0 = a.wa +
+                          ((size_t)e * a.rows + (size_t)tile * rows_per_block<MODE, FMT>()) *
+                              (size_t)K * kMats +
+                          (size_t)(2 * wc) * kFragElems + lane * 8;
+    const uint16_t* pa1 = pa0 + kFragElems;
     // MXFP4: the wave's two tiles are one packed band (up: 16 rows of W1
     // and W3; down: 32 rows of W2) of nslot slots, 64 code pieces and 16
     // scale dwords a slot.
@@ -326,9 +336,9 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     auto ring_load = [&](const int i, const int si) {
       if constexpr (FMT == kBf16) {
         ring0[i] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(pa0 + (size_t)si * kFragElems));
+            reinterpret_cast<const u32x4*>(pa0 + (size_t)si * step_elems));
         ring1[i] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(pa1 + (size_t)si * kFragElems));
+            reinterpret_cast<const u32x4*>(pa1 + (size_t)si * step_elems));
       } else {
         ring0[i] = __builtin_nontemporal_load(&pq[(size_t)si * 64]);
         rsc[i] = __builtin_nontemporal_load(&ps[(size_t)si * 16]);
@@ -656,21 +666,21 @@ int check_ffn_common(const moe_dims& d, const int32_t* offsets, const int32_t* p
 
 }  // namespace
 
-extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w1, const uint16_t* w3,
-                                 const int32_t* offsets, const int32_t* perm_token,
+extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w13, const int32_t* offsets,
+                                 const int32_t* perm_token,
                                  const int32_t* union_ids, const int32_t* union_size, moe_dims d,
                                  void* ws, size_t ws_bytes, void* stream) {
   using namespace eldr_host;
   int st = check_dims(d);
   if (st != MOE_OK) return st;
   if (d.T == 0) return MOE_OK;
-  if (!x || !w1 || !w3 || !ws) return MOE_ERR_INVALID;
+  if (!x || !w13 || !ws) return MOE_ERR_INVALID;
   st = check_ffn_common(d, offsets, perm_token, union_ids, union_size);
   if (st != MOE_OK) return st;
-  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w1, w3, offsets, perm_token, union_ids,
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids,
                    union_size, ws, d.I, d.H, 0, 0, 1, d.E, nullptr, nullptr};
   up.tiles = (d.I + eldr::rows_per_block<eldr::kUp, eldr::kBf16>() - 1) /
              eldr::rows_per_block<eldr::kUp, eldr::kBf16>();
@@ -691,7 +701,7 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   if (st != MOE_OK) return st;
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
-  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, nullptr, offsets, perm_token,
+  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, offsets, perm_token,
                      union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E, nullptr, nullptr};
   down.tiles =
       (d.H + eldr::rows_per_block<eldr::kDown, eldr::kBf16>() - 1) /
@@ -701,8 +711,8 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   return launch_status();
 }
 
-extern "C" int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t* w3,
-                              const uint16_t* w2, const int32_t* offsets,
+extern "C" int moe_expert_ffn(const float* x, const uint16_t* w13, const uint16_t* w2,
+                              const int32_t* offsets,
                               const int32_t* perm_token, const int32_t* union_ids,
                               const int32_t* union_size, moe_dims d, float* y_perm, void* ws,
                               size_t ws_bytes, void* stream) {
@@ -710,16 +720,14 @@ extern "C" int moe_expert_ffn(const float* x, const uint16_t* w1, const uint16_t
   int st = check_dims(d);
   if (st != MOE_OK) return st;
   if (d.T == 0) return MOE_OK;
-  if (!x || !w1 || !w3 || !w2 || !y_perm || !ws) return MOE_ERR_INVALID;
+  if (!x || !w13 || !w2 || !y_perm || !ws) return MOE_ERR_INVALID;
   st = check_ffn_common(d, offsets, perm_token, union_ids, union_size);
   if (st != MOE_OK) return st;
-  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y_perm) ||
-      !aligned16(ws))
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(y_perm) || !aligned16(ws))
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   float* h = static_cast<float*>(ws);
-  st = moe_expert_ffn_up(x, w1, w3, offsets, perm_token, union_ids, union_size, d, h, ws_bytes,
-                         stream);
+  st = moe_expert_ffn_up(x, w13, offsets, perm_token, union_ids, union_size, d, h, ws_bytes, stream);
   if (st != MOE_OK) return st;
   return moe_expert_ffn_down(h, w2, offsets, perm_token, union_ids, union_size, d, ws_bytes,
                              y_perm, stream);
@@ -754,7 +762,7 @@ extern "C" int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes,
   if (!aligned16(x) || !aligned16(up_codes) || !aligned4(up_scales) || !aligned16(ws))
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
-  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, nullptr, offsets, perm_token,
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, offsets, perm_token,
                    union_ids, union_size, ws, d.I, d.H, 0, 0, 1, d.E,
                    reinterpret_cast<const eldr::u32x4*>(up_codes),
                    reinterpret_cast<const uint32_t*>(up_scales)};
@@ -780,7 +788,7 @@ extern "C" int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_cod
   if (!aligned16(ws) || !aligned16(down_codes) || !aligned4(down_scales) || !aligned16(y_perm))
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
-  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), nullptr, nullptr, offsets, perm_token,
+  eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), nullptr, offsets, perm_token,
                      union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E,
                      reinterpret_cast<const eldr::u32x4*>(down_codes),
                      reinterpret_cast<const uint32_t*>(down_scales)};

@@ -1,52 +1,85 @@
-// moe_pack_weights: lay expert weights out as MFMA fragments, once, off the
-// decode path.
+// moe_pack_up_weights / moe_pack_down_weights: lay the bf16 expert weights out
+// as the expert FFN streams them, once, off the decode path.
 //
-// The expert FFN reads each 16-row x 32-column tile of a weight matrix as one
-// MFMA A operand: lane l takes row (l % 16) and the 8 columns starting at
-// 8 * (l / 16).  In the row-major [out, in] layout those 64 lane pieces are 16
-// rows apart; packed, the 64 pieces of one tile are one contiguous 1 KB block
-// in lane order, and a 16-row band's tiles follow each other along the
-// reduction axis, so every load instruction of the FFN reads 1 KB of
-// consecutive memory.  Packing permutes bf16 values; it changes no value and
-// no byte count.
+// The FFN reads each 16-row x 32-column tile of a weight matrix as one MFMA A
+// operand: lane l takes row (l % 16) and the 8 columns starting at
+// 8 * (l / 16); packed, the 64 lane pieces of one tile are one contiguous
+// 1 KB fragment in lane order.  A workgroup item covers a band of rows (up:
+// 64 rows of W1 and the same 64 rows of W3; down: 128 rows of W2), one wave
+// per 16 rows of W1/W3 or per 32 rows of W2, each wave reading two fragments
+// per k-step.  The packed band puts, for each k-step, the fragments of all
+// its waves side by side -- wave by wave, the wave's two fragments in order
+// -- and the k-steps one after the other, so a workgroup streams one
+// contiguous stretch of memory per item.  On MI355X that streams markedly
+// faster than the same bytes as one stream per wave and matrix (a probe of
+// the access pattern: 6.8-6.9 against 4.7-5.2 TB/s at 512-1536 items).
+// Packing permutes bf16 values; it changes no value and no byte count.
 #include "common.hpp"
 
 namespace eldr {
 
 // One thread moves one 16-byte piece (8 bf16): piece index p enumerates the
-// packed array in order, and its source is computed from (tile, lane).
-__global__ __launch_bounds__(256) void pack_kernel(const u32x4* __restrict__ src, int64_t pieces,
-                                                   int R, int K, u32x4* __restrict__ dst) {
+// packed array in order.  up: fragment f of wave w is W1 (f = 0) or W3 (f = 1)
+// rows 64 b + 16 w + (l % 16); down: rows 128 b + 32 w + 16 f + (l % 16) of
+// W2.  A last band with fewer rows holds only its waves' fragments.
+__global__ __launch_bounds__(256) void pack_band_kernel(const u32x4* __restrict__ a,
+                                                        const u32x4* __restrict__ b,
+                                                        int64_t pieces, int R, int K, int up,
+                                                        u32x4* __restrict__ dst) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= pieces) return;
   const int lane = (int)(p & 63);
-  const int64_t tile = p >> 6;             // ((e * R/16) + band) * K/32 + step
+  const int64_t frag = p >> 6;
   const int nk = K / 32;
-  const int step = (int)(tile % nk);
-  const int64_t band = tile / nk;          // e * R/16 + row band
-  const int64_t row = band * 16 + (lane & 15);
+  const int band_rows = up ? 64 : 128;
+  const int wave_rows = up ? 16 : 32;
+  const int64_t per_expert = (int64_t)(up ? 2 : 1) * (R / 16) * nk;  // fragments per expert
+  const int64_t e = frag / per_expert;
+  const int64_t q = frag - e * per_expert;
+  const int64_t per_band = 8LL * nk;  // fragments of a full band
+  const int band = (int)(q / per_band);
+  const int64_t r = q - (int64_t)band * per_band;
+  const int rows_b = min(band_rows, R - band * band_rows);
+  const int frags_step = 2 * (rows_b / wave_rows);  // fragments of one k-step of this band
+  const int step = (int)(r / frags_step);
+  const int f2 = (int)(r - (int64_t)step * frags_step);
+  const int w = f2 >> 1;
+  const int f = f2 & 1;
+  const int row = band * band_rows + w * wave_rows + (up ? 0 : 16 * f) + (lane & 15);
+  const u32x4* src = (up && f) ? b : a;
   const int64_t col = (int64_t)step * 32 + 8 * (lane >> 4);
-  dst[p] = src[(row * K + col) / 8];
+  dst[p] = src[((e * R + row) * K + col) / 8];
+}
+
+static int pack_band(const uint16_t* a, const uint16_t* b, int32_t E, int32_t R, int32_t K, int up,
+                     uint16_t* dst, void* stream) {
+  using namespace eldr_host;
+  if (E < 0 || R < 0 || K < 0) return MOE_ERR_INVALID;
+  if (R % 32 != 0 || K % 32 != 0) return MOE_ERR_UNSUPPORTED;
+  const int64_t pieces = (int64_t)(up ? 2 : 1) * E * R * K / 8;
+  if (pieces == 0) return MOE_OK;
+  if (!a || !b || !dst) return MOE_ERR_INVALID;
+  if (!aligned16(a) || !aligned16(b) || !aligned16(dst)) return MOE_ERR_UNSUPPORTED;
+  if (a == dst || b == dst) return MOE_ERR_INVALID;
+  const int64_t blocks = (pieces + 255) / 256;
+  if (blocks > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
+  hipLaunchKernelGGL(pack_band_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                     reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const u32x4*>(a),
+                     reinterpret_cast<const u32x4*>(b), pieces, R, K, up,
+                     reinterpret_cast<u32x4*>(dst));
+  return launch_status();
 }
 
 }  // namespace eldr
 
-extern "C" int moe_pack_weights(const uint16_t* src, int32_t E, int32_t R, int32_t K,
-                                uint16_t* dst, void* stream) {
-  using namespace eldr_host;
-  if (E < 0 || R < 0 || K < 0) return MOE_ERR_INVALID;
-  if (R % 16 != 0 || K % 32 != 0) return MOE_ERR_UNSUPPORTED;
-  const int64_t pieces = (int64_t)E * R * K / 8;
-  if (pieces == 0) return MOE_OK;
-  if (!src || !dst) return MOE_ERR_INVALID;
-  if (!aligned16(src) || !aligned16(dst)) return MOE_ERR_UNSUPPORTED;
-  if (src == dst) return MOE_ERR_INVALID;
-  const int64_t blocks = (pieces + 255) / 256;
-  if (blocks > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
-  hipLaunchKernelGGL(eldr::pack_kernel, dim3((unsigned)blocks), dim3(256), 0,
-                     reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const eldr::u32x4*>(src),
-                     pieces, R, K, reinterpret_cast<eldr::u32x4*>(dst));
-  return launch_status();
+extern "C" int moe_pack_up_weights(const uint16_t* w1, const uint16_t* w3, int32_t E, int32_t I,
+                                   int32_t H, uint16_t* dst, void* stream) {
+  return eldr::pack_band(w1, w3, E, I, H, 1, dst, stream);
+}
+
+extern "C" int moe_pack_down_weights(const uint16_t* w2, int32_t E, int32_t H, int32_t I,
+                                     uint16_t* dst, void* stream) {
+  return eldr::pack_band(w2, w2, E, H, I, 0, dst, stream);
 }
 
 // ---- MXFP4 ---------------------------------------------------------------------

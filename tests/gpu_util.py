@@ -41,7 +41,7 @@ class Layer:
         if experts_on_host:
             self._host = tuple(synth.bf16_bits(w) for w in (self.w1, self.w3, self.w2))
         # the expert FFN streams weights packed into MFMA fragments
-        self.p1, self.p3, self.p2 = B.pack_expert_weights(self.w1, self.w3, self.w2)
+        self.p13, self.p2 = B.pack_expert_weights(self.w1, self.w3, self.w2)
         self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
         self.buf = B.LayerBuffers.allocate(self.d)
 
@@ -64,7 +64,7 @@ class Layer:
         if routing is not None:
             routing = (torch.from_numpy(np.ascontiguousarray(routing[0], np.int32)).cuda(),
                        torch.from_numpy(np.ascontiguousarray(routing[1], np.float32)).cuda())
-        B.moe_layer(self.x, self.wg, self.p1, self.p3, self.p2, self.d, self.buf, routing=routing)
+        B.moe_layer(self.x, self.wg, self.p13, self.p2, self.d, self.buf, routing=routing)
         torch.cuda.synchronize()
         return fetch(self.buf, self.d)
 

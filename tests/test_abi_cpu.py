@@ -18,7 +18,7 @@ def lib():
 def test_exports_every_declared_function(lib):
     names = B.header_functions()
     assert {"moe_gate_topk", "moe_bucket", "moe_expert_ffn", "moe_expert_ffn_up",
-            "moe_expert_ffn_down", "moe_combine", "moe_pack_weights",
+            "moe_expert_ffn_down", "moe_combine", "moe_pack_up_weights", "moe_pack_down_weights",
             "moe_ffn_workspace_bytes", "moe_status_string", "moe_abi_version",
             "moe_sig_capture", "moe_sig_reset", "moe_sig_request_counts",
             "moe_stream_read_probe"} <= set(names)
@@ -57,7 +57,7 @@ def test_dims_rejected_by_every_call(lib, dims, status):
     s = None
     assert lib.moe_gate_topk(FAKE, FAKE, d, FAKE, FAKE, FAKE, s) == status
     assert lib.moe_bucket(FAKE, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, s) == status
-    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
                               1 << 40, s) == status
     assert lib.moe_combine(FAKE, FAKE, FAKE, d, FAKE, s) == status
 
@@ -66,7 +66,7 @@ def test_null_pointers_rejected(lib):
     d = B.dims(*GOOD)
     assert lib.moe_gate_topk(None, FAKE, d, FAKE, FAKE, FAKE, None) == B.MOE_ERR_INVALID
     assert lib.moe_bucket(FAKE, d, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.MOE_ERR_INVALID
-    assert lib.moe_expert_ffn(FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+    assert lib.moe_expert_ffn(FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
                               1 << 40, None) == B.MOE_ERR_INVALID
     assert lib.moe_combine(FAKE, FAKE, FAKE, d, None, None) == B.MOE_ERR_INVALID
 
@@ -74,7 +74,7 @@ def test_null_pointers_rejected(lib):
 def test_misaligned_pointers_rejected(lib):
     d = B.dims(*GOOD)
     assert lib.moe_gate_topk(FAKE_MIS, FAKE, d, FAKE, FAKE, FAKE, None) == B.MOE_ERR_UNSUPPORTED
-    assert lib.moe_expert_ffn(FAKE, FAKE_MIS, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+    assert lib.moe_expert_ffn(FAKE, FAKE_MIS, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
                               1 << 40, None) == B.MOE_ERR_UNSUPPORTED
     assert lib.moe_combine(FAKE_MIS, FAKE, FAKE, d, FAKE, None) == B.MOE_ERR_UNSUPPORTED
     odd = ctypes.c_void_p(0x10002)
@@ -84,7 +84,7 @@ def test_misaligned_pointers_rejected(lib):
 def test_workspace_too_small_rejected(lib):
     d = B.dims(*GOOD)
     need = B.moe_ffn_workspace_bytes(d)
-    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
+    assert lib.moe_expert_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE, FAKE,
                               need - 1, None) == B.MOE_ERR_WORKSPACE
 
 
@@ -98,7 +98,7 @@ def test_empty_batch_is_a_no_op(lib):
     # T = 0: gate, ffn and combine return before any launch.
     d = B.dims(0, 2048, 128, 8, 768)
     assert lib.moe_gate_topk(None, None, d, None, None, None, None) == B.MOE_OK
-    assert lib.moe_expert_ffn(None, None, None, None, None, None, None, None, d, None, None, 0,
+    assert lib.moe_expert_ffn(None, None, None, None, None, None, None, d, None, None, 0,
                               None) == B.MOE_OK
     assert lib.moe_combine(None, None, None, d, None, None) == B.MOE_OK
 
@@ -113,13 +113,18 @@ def test_binding_requires_device_tensors():
 
 def test_pack_arguments_rejected(lib):
     FAKE2 = ctypes.c_void_p(0x20000)
-    assert lib.moe_pack_weights(FAKE, -1, 16, 32, FAKE2, None) == B.MOE_ERR_INVALID
-    assert lib.moe_pack_weights(FAKE, 2, 24, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED   # R % 16
-    assert lib.moe_pack_weights(FAKE, 2, 16, 48, FAKE2, None) == B.MOE_ERR_UNSUPPORTED   # K % 32
-    assert lib.moe_pack_weights(None, 2, 16, 32, FAKE2, None) == B.MOE_ERR_INVALID
-    assert lib.moe_pack_weights(FAKE, 2, 16, 32, FAKE, None) == B.MOE_ERR_INVALID       # in place
-    assert lib.moe_pack_weights(FAKE_MIS, 2, 16, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED
-    assert lib.moe_pack_weights(None, 0, 16, 32, None, None) == B.MOE_OK                # empty
+    up, down = lib.moe_pack_up_weights, lib.moe_pack_down_weights
+    assert up(FAKE, FAKE, -1, 32, 32, FAKE2, None) == B.MOE_ERR_INVALID
+    assert up(FAKE, FAKE, 2, 48, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED    # I % 32
+    assert up(FAKE, FAKE, 2, 32, 48, FAKE2, None) == B.MOE_ERR_UNSUPPORTED    # H % 32
+    assert up(FAKE, None, 2, 32, 32, FAKE2, None) == B.MOE_ERR_INVALID
+    assert up(FAKE, FAKE2, 2, 32, 32, FAKE2, None) == B.MOE_ERR_INVALID       # in place
+    assert up(FAKE_MIS, FAKE, 2, 32, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED
+    assert up(None, None, 0, 32, 32, None, None) == B.MOE_OK                  # empty
+    assert down(FAKE, 2, 48, 32, FAKE2, None) == B.MOE_ERR_UNSUPPORTED        # H % 32
+    assert down(None, 2, 32, 32, FAKE2, None) == B.MOE_ERR_INVALID
+    assert down(FAKE, 2, 32, 32, FAKE, None) == B.MOE_ERR_INVALID             # in place
+    assert down(None, 2, 32, 0, None, None) == B.MOE_OK                       # empty
 
 
 def test_signature_calls_validate_on_host(lib):

@@ -163,9 +163,9 @@ def test_mxfp4_equals_bf16_path_on_dequantized_weights():
         wf = MX.dequantize(*q[name]).astype(np.float32)     # exact: every value is a bf16 number
         assert not (wf.view(np.uint32) & 0xFFFF).any()
         bf.append(torch.from_numpy(wf).cuda().to(torch.bfloat16))
-    p1, p3, p2 = B.pack_expert_weights(*bf)
+    p13, p2 = B.pack_expert_weights(*bf)
     buf = B.LayerBuffers.allocate(layer.d)
-    B.moe_layer(layer.x, layer.wg, p1, p3, p2, layer.d, buf)
+    B.moe_layer(layer.x, layer.wg, p13, p2, layer.d, buf)
     torch.cuda.synchronize()
     r = G.fetch(buf, layer.d)
     assert np.array_equal(r["ids"], g["ids"])

@@ -171,8 +171,8 @@ def test_empty_batch():
     buf.union_size.fill_(77)
     buf.counts.fill_(5)
     x = torch.empty((0, TINY.H), device="cuda")
-    w1, w3, w2 = B.pack_expert_weights(*synth.expert_weights(TINY, device="cuda"))
-    B.moe_layer(x, torch.zeros((TINY.E, TINY.H), device="cuda"), w1, w3, w2, d, buf)
+    w13, w2 = B.pack_expert_weights(*synth.expert_weights(TINY, device="cuda"))
+    B.moe_layer(x, torch.zeros((TINY.E, TINY.H), device="cuda"), w13, w2, d, buf)
     torch.cuda.synchronize()
     assert int(buf.union_size.item()) == 0
     assert int(buf.counts.abs().sum().item()) == 0
@@ -256,7 +256,7 @@ def test_graph_replay_matches_eager():
     G.say("case: qwen layer T=64 gate-routed, HIP graph replays vs eager")
     layer = G.Layer(QWEN, 64, experts_on_host=False)
     d, buf = layer.d, layer.buf
-    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p1, layer.p3, layer.p2, d, buf)  # noqa: E731
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf)  # noqa: E731
     run()
     torch.cuda.synchronize()
     eager = buf.out.clone()
@@ -305,7 +305,7 @@ def test_graph_replay_large_batch_token_groups():
     _full_check(layer, g0, False, routing=(ids.astype(np.int64), w))
     d, buf = layer.d, layer.buf
     r = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
-    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p1, layer.p3, layer.p2, d, buf, routing=r)  # noqa: E731
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r)  # noqa: E731
     eager = buf.out.clone()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -338,17 +338,40 @@ def test_batch_of_65_tokens_crosses_the_group_boundary():
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
-@pytest.mark.parametrize("E,R,K", [(3, 16, 32), (2, 48, 96), (128, 768, 2048), (5, 2880, 2880)])
-def test_pack_weights_is_the_documented_permutation(E, R, K):
-    G.say(f"case: pack E={E} R={R} K={K}")
+def _band_reference(srcs, band_rows: int, wave_rows: int) -> np.ndarray:
+    """The documented packed order, built band by band: per expert, band, k-step,
+    wave and its two fragments, the 64 lane pieces (lane l: row l % 16, values
+    8 (l // 16) .. + 7 of the k-step).  srcs: one [E, R, K] array per fragment
+    kind (up: W1, W3 for fragments 0, 1) or a single array whose fragment f is
+    the wave's f-th 16-row tile (down)."""
+    E, R, K = srcs[0].shape
+    nk = K // 32
+    bands = []
+    for b in range((R + band_rows - 1) // band_rows):
+        waves = min(band_rows, R - b * band_rows) // wave_rows
+        blk = np.empty((E, nk, waves, 2, 64, 8), np.uint16)
+        for w in range(waves):
+            for f in range(2):
+                src = srcs[f] if len(srcs) == 2 else srcs[0]
+                r0 = b * band_rows + w * wave_rows + (0 if len(srcs) == 2 else 16 * f)
+                tile = src[:, r0:r0 + 16, :].reshape(E, 16, nk, 4, 8).transpose(0, 2, 3, 1, 4)
+                blk[:, :, w, f] = tile.reshape(E, nk, 64, 8)
+        bands.append(blk.reshape(E, -1))
+    return np.concatenate(bands, axis=1).reshape(-1)
+
+
+@pytest.mark.parametrize("E,I,H", [(3, 32, 32), (2, 96, 64), (128, 768, 2048), (2, 2880, 2880)])
+def test_pack_weights_are_the_documented_permutation(E, I, H):
+    # I = 32 and 96 and H = 2880 leave a short last band (2 of 4 waves).
+    G.say(f"case: pack up and down, E={E} I={I} H={H}")
     g = torch.Generator(device="cuda")
-    g.manual_seed(E * 1000 + R)
-    w = torch.randn((E, R, K), generator=g, device="cuda").to(torch.bfloat16)
-    packed = synth.bf16_bits(B.moe_pack_weights(w))
-    src = synth.bf16_bits(w)
-    # fragment (e, band, step) holds, lane by lane, src[e, 16 band + l % 16, 32 step + 8 (l // 16) + j]
-    ref = src.reshape(E, R // 16, 16, K // 32, 4, 8).transpose(0, 1, 3, 4, 2, 5).reshape(-1)
-    assert np.array_equal(packed.reshape(-1), ref)
+    g.manual_seed(E * 1000 + I)
+    w1, w3 = (torch.randn((E, I, H), generator=g, device="cuda").to(torch.bfloat16) for _ in range(2))
+    w2 = torch.randn((E, H, I), generator=g, device="cuda").to(torch.bfloat16)
+    up = synth.bf16_bits(B.moe_pack_up_weights(w1, w3))
+    assert np.array_equal(up.reshape(-1), _band_reference([synth.bf16_bits(w1), synth.bf16_bits(w3)], 64, 16))
+    down = synth.bf16_bits(B.moe_pack_down_weights(w2))
+    assert np.array_equal(down.reshape(-1), _band_reference([synth.bf16_bits(w2)], 128, 32))
 
 
 def test_stream_probe_reads_without_writing():
