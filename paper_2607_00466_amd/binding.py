@@ -402,14 +402,16 @@ class LayerBuffers:
         )
 
 
-def _gate_and_bucket(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream) -> None:
+def _gate_and_bucket(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream):
+    """Gate (unless routing is given) and buckets; returns the routing weights to combine with."""
     if routing is None:
         moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
+        ids, w = buf.topk_ids, buf.topk_w
     else:
-        buf.topk_ids.copy_(routing[0])
-        buf.topk_w.copy_(routing[1])
-    moe_bucket(buf.topk_ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
-               buf.union_ids, buf.union_size, stream)
+        ids, w = routing
+    moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
+               buf.union_size, stream)
+    return w
 
 
 def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
@@ -417,22 +419,23 @@ def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, s
 
     w13 and w2 are the expert weights packed by ``pack_expert_weights``.
 
-    ``routing=(topk_ids, topk_w)`` bypasses the gate (the ids are copied into
-    ``buf``).  Returns ``buf.out``.
+    ``routing=(topk_ids, topk_w)`` (int32 [T, K] and fp32 [T, K] device
+    tensors) bypasses the gate: the bucket and the combine read them in place.
+    Returns ``buf.out``.
     """
-    _gate_and_bucket(x, w_gate, d, buf, routing, stream)
+    w = _gate_and_bucket(x, w_gate, d, buf, routing, stream)
     moe_expert_ffn(x, w13, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
                    buf.y_perm, buf.ws, stream)
-    moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
+    moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 
 
 def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
     """moe_layer with MXFP4 experts: ``up`` and ``down`` from pack_mxfp4_expert_weights."""
-    _gate_and_bucket(x, w_gate, d, buf, routing, stream)
+    w = _gate_and_bucket(x, w_gate, d, buf, routing, stream)
     moe_expert_ffn_mxfp4(x, up, down, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
                          d, buf.y_perm, buf.ws, stream)
-    moe_combine(buf.y_perm, buf.pair_pos, buf.topk_w, d, buf.out, stream)
+    moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 
 
