@@ -219,14 +219,18 @@ int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offse
  *
  * moe_pack_mxfp4_up / moe_pack_mxfp4_down -- permute the unpacked W1 and W3
  * ([E, I, H]) or W2 ([E, H, I]) into the layout the MXFP4 FFN streams, once,
- * off the decode path.  For each expert, band (up: 16 rows of W1 and the same
- * 16 rows of W3; down: 32 rows of W2), slot s of two k-steps (64 values:
- * H/64 slots up, I/64 down) and lane l (0 .. 63), 16 bytes: the 4 code bytes
+ * off the decode path.  A wave band is 16 rows of W1 and the same 16 rows of
+ * W3 (up), or 32 rows of W2 (down); a workgroup band is 4 consecutive wave
+ * bands (the last one of an expert may hold fewer).  A slot s is two k-steps
+ * (64 values: H/64 slots up, I/64 down).  For each expert, workgroup band,
+ * slot, wave band within it and lane l (0 .. 63), 16 bytes: the 4 code bytes
  * of row l % 16 and values 64 s + 8 (l / 16) .. + 7, then the same for
- * 64 s + 32 + 8 (l / 16), of tile 0 (up: W1; down: the band's first 16
- * rows), then both again for tile 1 (up: W3; down: the band's last 16 rows).
- * Scales: for each expert, band and slot, 16 dwords (row 0 .. 15), each the
- * 4 scale bytes in that same order.  codes receives E*I*H bytes (up) or
+ * 64 s + 32 + 8 (l / 16), of tile 0 (up: W1; down: the wave band's first 16
+ * rows), then both again for tile 1 (up: W3; down: its last 16 rows).
+ * Scales: in the same (expert, workgroup band, slot, wave band) order, 16
+ * dwords (row 0 .. 15), each the 4 scale bytes in that same order.  A
+ * workgroup item thus reads one contiguous stretch of codes and one of
+ * scales.  codes receives E*I*H bytes (up) or
  * E*H*I/2 (down), scales E*I*H/16 (up) or E*H*I/32 (down): the unpacked
  * sizes.  Inputs and outputs are distinct device buffers; code inputs and
  * scale outputs 4-byte aligned, code outputs 16-byte aligned.  Requires

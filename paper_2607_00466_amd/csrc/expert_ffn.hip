@@ -260,6 +260,8 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
   constexpr int kRing = ring_depth<FMT, NT>();
   constexpr int kSlot = slot_steps<FMT>();  // k-steps per ring slot
   constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
+  static_assert(ffn_waves<MODE, FMT>() == 4,
+                "the packed weight layouts put 4 waves' fragments side by side per band");
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
   __shared__ int tok[kGroupTokens];
 
@@ -295,9 +297,6 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     const int r0 = tile * rows_per_block<MODE, FMT>() + wave * (MODE == kUp ? 16 : 32);
     const bool ok0 = r0 < a.rows;
     const bool ok1 = MODE == kUp ? ok0 : (r0 + 16 < a.rows);
-    // MXFP4: a 16-row tile past the end of the matrix (only when rows is not
-    // a multiple of the band) re-reads the band's first tile and is not stored.
-    const int ra0 = ok0 ? r0 : tile * rows_per_block<MODE, FMT>();
 
     // A operand: lane holds row (lane % 16) of its 16-row tile, k-group
     // (lane / 16).  bf16 weights are packed by band (moe_pack_up_weights,
@@ -317,13 +316,18 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
                               (size_t)K * kMats +
                           (size_t)(2 * wc) * kFragElems + lane * 8;
     const uint16_t* pa1 = pa0 + kFragElems;
-    // MXFP4: the wave's two tiles are one packed band (up: 16 rows of W1
-    // and W3; down: 32 rows of W2) of nslot slots, 64 code pieces and 16
-    // scale dwords a slot.
+    // MXFP4: the wave's two tiles are one wave band (up: 16 rows of W1 and
+    // W3; down: 32 rows of W2), 64 code pieces and 16 scale dwords a slot;
+    // the workgroup band's wave bands lie side by side slot by slot
+    // (moe_pack_mxfp4_up / _down), and a wave past a short last band re-reads
+    // the band's last wave band.
     constexpr int kBandRows = MODE == kUp ? 16 : 32;
-    const size_t qband = (size_t)e * (a.rows / kBandRows) + ra0 / kBandRows;
-    const u32x4* pq = a.qcodes + qband * nslot * 64 + lane;
-    const uint32_t* ps = a.qscales + qband * nslot * 16 + arow;
+    const int nwb = a.rows / kBandRows;
+    const int wb_q = min(rows_per_block<MODE, FMT>() / kBandRows, nwb - tile * (rows_per_block<MODE, FMT>() / kBandRows));
+    const size_t q0 = ((size_t)e * nwb + (size_t)tile * (rows_per_block<MODE, FMT>() / kBandRows)) * nslot +
+                      (size_t)min(wave, wb_q - 1);
+    const u32x4* pq = a.qcodes + q0 * 64 + lane;
+    const uint32_t* ps = a.qscales + q0 * 16 + arow;
 
     // Weight ring: slot i holds the weights of the ring slot congruent to i
     // mod kRing.  Loads past the last slot re-read the last one (always
@@ -340,8 +344,8 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
         ring1[i] = __builtin_nontemporal_load(
             reinterpret_cast<const u32x4*>(pa1 + (size_t)si * step_elems));
       } else {
-        ring0[i] = __builtin_nontemporal_load(&pq[(size_t)si * 64]);
-        rsc[i] = __builtin_nontemporal_load(&ps[(size_t)si * 16]);
+        ring0[i] = __builtin_nontemporal_load(&pq[(size_t)si * wb_q * 64]);
+        rsc[i] = __builtin_nontemporal_load(&ps[(size_t)si * wb_q * 16]);
       }
     };
     auto ring_prologue = [&](auto N_) {

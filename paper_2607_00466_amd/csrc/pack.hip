@@ -90,25 +90,35 @@ extern "C" int moe_pack_down_weights(const uint16_t* w2, int32_t E, int32_t H, i
 // 8 * (l / 16) of each k-step, whose FP4 codes are 4 consecutive bytes of the
 // row.  Its 16 bytes are (tile 0, step 0), (tile 0, step 1), (tile 1, step
 // 0), (tile 1, step 1).  The 16 rows' E8M0 scales of the slot follow the same
-// order, one dword per row.  Up pairs W1 and W3 rows of a 16-row band; down
-// pairs the two 16-row halves of a 32-row band of W2.
+// order, one dword per row.  Up pairs W1 and W3 rows of a 16-row wave band;
+// down pairs the two 16-row halves of a 32-row wave band of W2.  The four
+// wave bands of a workgroup band lie side by side slot by slot, as for bf16.
 
 namespace eldr {
 
 // One thread moves one lane piece (16 bytes of codes); the threads of lanes
 // 0 .. 15 also move their row's scale dword.  p enumerates the packed codes
-// as ((band * nslot) + slot) * 64 + lane over all bands of all experts.
+// in their packed order: per expert, workgroup band of 4 wave bands (the last
+// one may hold fewer), slot, wave band within it, lane.  A wave band is 16
+// rows (up) or 32 rows (down), so a workgroup item's codes are one
+// contiguous stretch and its scales another.
 __global__ __launch_bounds__(256) void pack_mxfp4_kernel(
     const uint32_t* __restrict__ ca, const uint32_t* __restrict__ cb,
-    const uint8_t* __restrict__ sa, const uint8_t* __restrict__ sb, int64_t pieces, int K,
+    const uint8_t* __restrict__ sa, const uint8_t* __restrict__ sb, int64_t pieces, int R, int K,
     int band_rows, u32x4* __restrict__ dq, uint32_t* __restrict__ ds) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= pieces) return;
   const int lane = (int)(p & 63);
-  const int64_t bs = p >> 6;  // band * nslot + slot
+  const int64_t q = p >> 6;  // (slot, wave band) unit in packed order
   const int nslot = K / 64;
-  const int slot = (int)(bs % nslot);
-  const int64_t band = bs / nslot;
+  const int nwb = R / band_rows;  // wave bands per expert
+  const int64_t e = q / ((int64_t)nwb * nslot);
+  const int64_t rq = q - e * nwb * nslot;
+  const int j = (int)(rq / (4 * nslot));          // workgroup band
+  const int r2 = (int)(rq - (int64_t)j * 4 * nslot);
+  const int wb = min(4, nwb - 4 * j);             // wave bands in this workgroup band
+  const int slot = r2 / wb;
+  const int64_t band = e * nwb + 4 * j + (r2 - slot * wb);  // wave band in [E * R / band_rows]
   const int r = lane & 15;
   const int g = lane >> 4;
   // source rows of the two tiles, in the flattened [E * R] row order
@@ -130,7 +140,7 @@ __global__ __launch_bounds__(256) void pack_mxfp4_kernel(
     const uint32_t b1 = sa[row0 * nb + k0 + 1];
     const uint32_t b2 = s1[row1 * nb + k0];
     const uint32_t b3 = s1[row1 * nb + k0 + 1];
-    ds[bs * 16 + r] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+    ds[q * 16 + r] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
   }
 }
 
@@ -154,7 +164,7 @@ int pack_mxfp4(const uint8_t* ca, const uint8_t* sa, const uint8_t* cb, const ui
   if (blocks > 0x7fffffffLL) return MOE_ERR_UNSUPPORTED;
   hipLaunchKernelGGL(eldr::pack_mxfp4_kernel, dim3((unsigned)blocks), dim3(256), 0,
                      reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const uint32_t*>(ca),
-                     reinterpret_cast<const uint32_t*>(cb), sa, sb, pieces, K, band_rows,
+                     reinterpret_cast<const uint32_t*>(cb), sa, sb, pieces, R, K, band_rows,
                      reinterpret_cast<eldr::u32x4*>(codes), reinterpret_cast<uint32_t*>(scales));
   return launch_status();
 }

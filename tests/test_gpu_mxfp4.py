@@ -81,6 +81,15 @@ def _dwords(a: np.ndarray) -> np.ndarray:
     return np.ascontiguousarray(a).view(np.uint32)
 
 
+def _wg_bands(per_band: np.ndarray) -> np.ndarray:
+    """Regroup [E, wave band, slot, ...] into the packed order: per expert, groups
+    of 4 wave bands (the last may hold fewer), slot, wave band within the group."""
+    E, nwb = per_band.shape[:2]
+    parts = [np.swapaxes(per_band[:, j:j + 4], 1, 2).reshape(E, -1) for j in range(0, nwb, 4)]
+    return np.concatenate(parts, axis=1).reshape(-1)
+
+
+# H = 64, 320 and 2880 leave a short last workgroup band of W2 (2 of 4 wave bands).
 @pytest.mark.parametrize("E,I,H", [(3, 64, 64), (2, 192, 320), (4, 2880, 2880)])
 def test_pack_mxfp4_is_the_documented_permutation(E, I, H):
     G.say(f"case: MXFP4 pack E={E} I={I} H={H}")
@@ -92,22 +101,23 @@ def test_pack_mxfp4_is_the_documented_permutation(E, I, H):
     (uc, us), (dc, ds) = B.pack_mxfp4_expert_weights(w1, w3, w2)
     torch.cuda.synchronize()
     h = lambda t: t.cpu().numpy()
-    # up codes: per (expert, 16-row band, slot of 2 k-steps), lane = 16 g + r holds the dwords
-    # (W1 step 0, W1 step 1, W3 step 0, W3 step 1) of row r, k-group g
+    # up codes: per (expert, 16-row wave band, slot of 2 k-steps), lane = 16 g + r holds the
+    # dwords (W1 step 0, W1 step 1, W3 step 0, W3 step 1) of row r, k-group g; the wave
+    # bands of a workgroup band (4 of them) lie side by side slot by slot
     ns = H // 64
     parts = [_dwords(h(c)).reshape(E, I // 16, 16, ns, 2, 4) for c in (w1[0], w3[0])]
     ref = np.stack([p.transpose(0, 1, 3, 5, 2, 4) for p in parts], axis=-2)  # [E,nb,ns,g,r,m,j]
-    assert np.array_equal(_dwords(h(uc)), ref.reshape(-1))
+    assert np.array_equal(_dwords(h(uc)), _wg_bands(ref))
     parts = [h(s).reshape(E, I // 16, 16, ns, 2) for s in (w1[1], w3[1])]
     ref = np.stack([p.transpose(0, 1, 3, 2, 4) for p in parts], axis=-2)       # [E,nb,ns,r,m,j]
-    assert np.array_equal(h(us), ref.reshape(-1))
+    assert np.array_equal(h(us), _wg_bands(ref))
     # down: the two 16-row halves of each 32-row band of W2
     ns = I // 64
     p = _dwords(h(w2[0])).reshape(E, H // 32, 2, 16, ns, 2, 4)
     ref = p.transpose(0, 1, 4, 6, 3, 2, 5)                                      # [E,nb,ns,g,r,m,j]
-    assert np.array_equal(_dwords(h(dc)), ref.reshape(-1))
+    assert np.array_equal(_dwords(h(dc)), _wg_bands(ref))
     p = h(w2[1]).reshape(E, H // 32, 2, 16, ns, 2)
-    assert np.array_equal(h(ds), p.transpose(0, 1, 4, 3, 2, 5).reshape(-1))
+    assert np.array_equal(h(ds), _wg_bands(p.transpose(0, 1, 4, 3, 2, 5)))
 
 
 # ---------------------------------------------------------------------------- FFN parity
