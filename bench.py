@@ -189,6 +189,16 @@ class Bench:
         t1.record(self.stream)
         torch.cuda.synchronize()
         layer_ms = t0.elapsed_time(t1) / steps
+        # Spread: events between consecutive replays of the full graph (a
+        # separate pass), each replay's time divided by its layer steps.
+        n_rep = max(2, steps // per)
+        rev = [torch.cuda.Event(enable_timing=True) for _ in range(n_rep + 1)]
+        rev[0].record(self.stream)
+        for i in range(n_rep):
+            full.replay()
+            rev[i + 1].record(self.stream)
+        torch.cuda.synchronize()
+        per_layer = np.array([rev[i].elapsed_time(rev[i + 1]) for i in range(n_rep)]) / per
         del full, tails
         # Per-kernel durations of the FFN halves, with events around each
         # launch on the stream it runs on (a separate eager pass, so the
@@ -201,7 +211,8 @@ class Bench:
         up = np.array([e[0].elapsed_time(e[1]) for e in evs])
         down = np.array([e[1].elapsed_time(e[2]) for e in evs])
         return {"layer_ms": layer_ms, "up_ms": float(up.mean()), "down_ms": float(down.mean()),
-                "up_ms_median": float(np.median(up)), "down_ms_median": float(np.median(down))}
+                "up_ms_median": float(np.median(up)), "down_ms_median": float(np.median(down)),
+                "layer_ms_p10_p50_p90": [float(np.percentile(per_layer, q)) for q in (10, 50, 90)]}
 
 
 class MxBench(Bench):
@@ -378,15 +389,15 @@ def calibration(reps: int = 10) -> dict:
             "how": "best of 10: moe_stream_read_probe (non-temporal loads) over 2 GiB; a 2 GiB device copy"}
 
 
-def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:
-    """The float64 oracle on the host, one BLAS thread, on the same layer."""
+def cpu_baseline(bench: Bench, U: int, budget_s: float, threads: int = 1) -> dict:
+    """The float64 oracle on the host, `threads` BLAS threads, on the same layer."""
     from threadpoolctl import threadpool_limits
 
     from oracle import moe_oracle
 
     w1, w3, w2 = (synth.bf16_bits(w) for w in bench.raw_weights)
     runs, t_total = 0, 0.0
-    with threadpool_limits(limits=1):
+    with threadpool_limits(limits=threads):
         while t_total < budget_s and runs < 50:
             t = time.perf_counter()
             moe_oracle.moe_layer(bench.x_np, bench.wg_np, w1, w3, w2, bench.shape.K)
@@ -396,11 +407,20 @@ def cpu_baseline(bench: Bench, U: int, budget_s: float) -> dict:
     return {
         "value": layer_bytes(bench.shape, bench.T, U, True) / per_layer / 1e9,
         "unit": "GB/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
         "sample": f"{runs} runs of the whole gate-routed layer (same inputs), float64 NumPy, "
                   f"{per_layer * 1e3:.0f} ms per layer, {os.cpu_count()} host cores visible",
     }
+
+
+def host_threads() -> int:
+    """Threads the host lets this process use (its affinity), at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def sweep(path: str, steps: int, warmup: int) -> None:
@@ -436,6 +456,17 @@ def sweep(path: str, steps: int, warmup: int) -> None:
         f.write(json.dumps({"fit": "layer_us = a + b * U", "a_us": a, "b_us_per_expert": b,
                             "r2": r2, "per_expert_GBps": shape.expert_bytes / b / 1e3}) + "\n")
     log(f"fit: t = {a:.2f} + {b:.3f} U us (R^2 {r2:.4f})")
+    # The paper's motivating figure, for context only: on one MI300X with vLLM's
+    # MoE kernels the layer's latency rises 4.7x as the active experts go from
+    # 16 to 128 at decode batch 64 (Motivation, "Active Expert Count Drives MoE
+    # Decode Latency").  The same ratio here, largest realised union over U=16:
+    ratio = ts[-1] / ts[0]
+    with open(path, "a") as f:
+        f.write(json.dumps({"latency_ratio_largest_union_over_U16": ratio, "union_from": int(Us[0]),
+                            "union_to": int(Us[-1]), "paper_ratio_16_to_128": 4.7,
+                            "paper_hardware": "1x MI300X, vLLM MoE kernels (context, not a target)"})
+                + "\n")
+    log(f"latency ratio U={int(Us[-1])} / U={int(Us[0])}: {ratio:.2f} (paper, MI300X: 4.7 for 16 -> 128)")
 
 
 class MultiLayer:
@@ -854,6 +885,7 @@ def main() -> int:
                    "E": shape.E, "top_k": shape.K, "hidden": shape.H, "intermediate": shape.I,
                    "tokens": T, "union": U, "weight_copies": len(bench.weights)},
         "layer_us": round(r["layer_ms"] * 1e3, 2),
+        "layer_us_p10_p50_p90": [round(v * 1e3, 2) for v in r["layer_ms_p10_p50_p90"]],
         "layer_frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "ffn_up_us": round(r["up_ms"] * 1e3, 2),
         "ffn_down_us": round(r["down_ms"] * 1e3, 2),
@@ -867,6 +899,10 @@ def main() -> int:
     if args.cpu_seconds > 0:
         log("timing the CPU oracle ...")
         out["cpu_baseline"] = cpu_baseline(bench, U, args.cpu_seconds)
+        # secondary, for context: the same oracle with every host thread it may use
+        n = host_threads()
+        if n > 1:
+            out["cpu_baseline_all_threads"] = cpu_baseline(bench, U, args.cpu_seconds / 2, threads=n)
     del bench
     torch.cuda.empty_cache()
     if args.sweep:
