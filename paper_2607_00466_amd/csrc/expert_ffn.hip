@@ -15,10 +15,11 @@
 //   workgroup's loads of one k-step are adjacent, so an item is one
 //   contiguous stream.
 // * An expert with at most 64 tokens has one item per band, so its weights
-//   are read once.  A bigger bucket is split into token groups of 64 whose
-//   items for one band get adjacent workgroup slots on one XCD: they run side
-//   by side and the second read of the band is served mostly by that XCD's
-//   L2 rather than HBM.
+//   are read once, with non-temporal loads.  A bigger bucket is split into
+//   token groups of 64 whose items for one band get adjacent workgroup slots
+//   on one XCD: they run side by side, read the band with ordinary (cacheable)
+//   loads, and the second read is served mostly by that XCD's L2 rather than
+//   HBM.
 // * The item's tokens are gathered, carried as a pair of bf16 values (high
 //   part + rounded remainder) and staged in LDS in fixed-shape chunks,
 //   double-buffered, shared by the workgroup's four waves; each wave reads
@@ -291,7 +292,13 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
 
   // One item: the token group of up to kGroupTokens tokens starting at slot
   // s_begin + p0 of expert e's bucket, against row band `tile`.
-  auto run_item = [&](const int e, const int tile, const int s_begin, const int p0, const int c) {
+  // SHARED_: the band is read by more than one token group of the expert; those
+  // items run side by side on one XCD, so their weight loads are ordinary
+  // (cacheable) loads and the repeated reads are served by the XCD's L2.
+  // Every other band is read once, with non-temporal loads.
+  auto run_item = [&](auto SHARED_, const int e, const int tile, const int s_begin, const int p0,
+                      const int c) {
+    constexpr bool kShared = decltype(SHARED_)::value != 0;
     const int nt = (c + 15) / 16;
 
     const int r0 = tile * rows_per_block<MODE, FMT>() + wave * (MODE == kUp ? 16 : 32);
@@ -339,13 +346,25 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     // (a plain streaming read reaches about 7.0 TB/s this way, 6.2 without).
     auto ring_load = [&](const int i, const int si) {
       if constexpr (FMT == kBf16) {
-        ring0[i] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(pa0 + (size_t)si * step_elems));
-        ring1[i] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(pa1 + (size_t)si * step_elems));
+        const u32x4* q0 = reinterpret_cast<const u32x4*>(pa0 + (size_t)si * step_elems);
+        const u32x4* q1 = reinterpret_cast<const u32x4*>(pa1 + (size_t)si * step_elems);
+        if constexpr (kShared) {
+          ring0[i] = *q0;
+          ring1[i] = *q1;
+        } else {
+          ring0[i] = __builtin_nontemporal_load(q0);
+          ring1[i] = __builtin_nontemporal_load(q1);
+        }
       } else {
-        ring0[i] = __builtin_nontemporal_load(&pq[(size_t)si * wb_q * 64]);
-        rsc[i] = __builtin_nontemporal_load(&ps[(size_t)si * wb_q * 16]);
+        const u32x4* q = &pq[(size_t)si * wb_q * 64];
+        const uint32_t* r = &ps[(size_t)si * wb_q * 16];
+        if constexpr (kShared) {
+          ring0[i] = *q;
+          rsc[i] = *r;
+        } else {
+          ring0[i] = __builtin_nontemporal_load(q);
+          rsc[i] = __builtin_nontemporal_load(r);
+        }
       }
     };
     auto ring_prologue = [&](auto N_) {
@@ -562,7 +581,7 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     if (e < 0 || e >= a.experts) return;  // not reached for a union member
     const int s_begin = a.offsets[e];
     const int c = a.offsets[e + 1] - s_begin;
-    if (c > 0) run_item(e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
+    if (c > 0) run_item(Int<0>{}, e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
   } else {
     // Every wave builds the table of its XCD's experts in registers: lane m
     // holds expert m's id (union_ids is read together with union_size; it is
@@ -606,9 +625,14 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
       const int group = r - tile * g;
       const int p0 = group * kGroupTokens;
       const int c = min(kGroupTokens, __builtin_amdgcn_readlane(c_lane, m) - p0);
-      if (c > 0)
-        run_item(__builtin_amdgcn_readlane(e_lane, m), tile,
-                 __builtin_amdgcn_readlane(sb_lane, m), p0, c);
+      if (c > 0) {
+        const int ie = __builtin_amdgcn_readlane(e_lane, m);
+        const int isb = __builtin_amdgcn_readlane(sb_lane, m);
+        if (g > 1)
+          run_item(Int<1>{}, ie, tile, isb, p0, c);
+        else
+          run_item(Int<0>{}, ie, tile, isb, p0, c);
+      }
     }
   }
 }
