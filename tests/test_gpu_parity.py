@@ -129,6 +129,15 @@ def test_ragged_shape_partial_bands():
     _full_check(layer, layer.run(), True)
 
 
+def test_ragged_shape_even_steps_short_band():
+    # H = 320 (an even number of k-steps, 2.5 bands of W2) and I = 96 (a short
+    # last band of W1/W3), E not a multiple of 8, a 2-tile kernel (T = 21).
+    G.say("case: ragged shape E=13 top-3 H=320 I=96 T=21")
+    shape = synth.LayerShape("ragged_even", E=13, K=3, H=320, I=96)
+    layer = G.Layer(shape, 21, seed=6)
+    _full_check(layer, layer.run(), True)
+
+
 def test_k_equals_e():
     G.say("case: K = E = 16, H=256 I=128 T=5")
     shape = synth.LayerShape("k_eq_e", E=16, K=16, H=256, I=128)
