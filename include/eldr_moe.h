@@ -108,7 +108,11 @@ int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, float* logits
  *   perm_token [T*K]   token of each slot: experts ascending, and within an
  *                      expert tokens ascending
  *   pair_pos   [T*K]   pair_pos[t*K + j] = slot of (t, topk_ids[t, j])
- *   union_ids  [E]     experts with counts > 0 ascending, then -1 padding
+ *   union_ids  [E]     experts with counts > 0 in dispatch order -- more
+ *                      16-token tiles (ceil(count / 16)) first, equal ones by
+ *                      ascending id -- then -1 padding (moe_expert_ffn runs
+ *                      the largest buckets first and deals experts to XCDs
+ *                      in this order)
  *   union_size [1]     number of distinct experts U (stays on the device)
  * If an id is out of range or repeated within a token, union_size is set to
  * -1 and the other outputs are unspecified; moe_expert_ffn then does nothing.
@@ -164,6 +168,9 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * has at most 64 tokens; a bigger bucket is split into groups of 64 tokens
  * whose workgroups run side by side on one XCD and share that XCD's L2 for
  * the repeated weight reads.  Experts outside the union are never touched.
+ * Work follows the union's dispatch order (largest buckets first): with
+ * T <= 64 experts are dealt round-robin over the 8 XCDs, with T > 64 their
+ * (expert, row band) units are, so skewed buckets still load the XCDs evenly.
  * The grid is sized from E and T alone and reads union_size on the device,
  * so no host synchronisation is needed between moe_bucket and this call.
  *

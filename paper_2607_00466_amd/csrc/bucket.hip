@@ -4,19 +4,28 @@
 // Each expert gets a bitmap over tokens in LDS (bit t set when token t picked
 // it).  A slot's rank inside its bucket is the number of set bits below t,
 // so buckets list their tokens in ascending order without any sort, and the
-// result does not depend on the order in which threads ran.
+// result does not depend on the order in which threads ran.  The union is
+// listed in dispatch order: experts with more 16-token tiles (the expert
+// FFN's unit of work per item) first, equal ones by ascending id, so the FFN
+// starts its longest items first while batches of small buckets stream the
+// experts in address order.  An expert's position is the number of experts
+// with a larger (tiles, -id) key.
 #include "common.hpp"
 
 namespace eldr {
 
 constexpr int kBucketThreads = 1024;
 constexpr int kBucketMaxWords = 16384;  // E * ceil(T / 32) limit (64 KiB of bitmaps)
+constexpr int kOrderTokens = 16;        // union order: buckets compared in tiles of 16 tokens
 
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
     const int32_t* __restrict__ ids, int T, int E, int K, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token, int32_t* __restrict__ pair_pos,
     int32_t* __restrict__ union_ids, int32_t* __restrict__ union_size) {
   extern __shared__ uint32_t smem[];
+  // union order keys, larger first: 16-token tiles (<= 256) above 255 - e
+  // (e < 256); 0 past E, below every expert with tokens
+  __shared__ __attribute__((aligned(16))) int key_s[MOE_MAX_E];
   __shared__ int bad;
   __shared__ int total_pairs, total_union;
   const int W = (T + 31) / 32;
@@ -53,12 +62,37 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
       run += __popc(mask[e * W + w]);
     }
     cnt[e] = run;
+    key_s[e] = (((run + kOrderTokens - 1) / kOrderTokens) << 8) | (MOE_MAX_E - 1 - e);
   }
+  for (int e = E + tid; e < MOE_MAX_E; e += kBucketThreads) key_s[e] = 0;
   __syncthreads();
 
   // Exclusive scans of counts and of (counts > 0) over E <= 256 experts by
   // wave 0: 4 consecutive experts per lane, then a shuffle scan over lanes.
-  if (tid < kWave) {
+  // Meanwhile the other waves rank each expert: R adjacent threads split the
+  // keys (in runs of 4, read 16 bytes at a time) and sum their counts.
+  static_assert(kBucketThreads >= kWave + 2 * MOE_MAX_E, "two ranking threads an expert");
+  if (tid >= kWave) {
+    const int R = E <= (kBucketThreads - kWave) / 4 ? 4 : 2;
+    const int q = tid - kWave;
+    const int e = q / R;
+    const int quads = (E + 3) / 4;
+    const int per = (quads + R - 1) / R;
+    const int q0 = (q % R) * per;
+    const int q1 = min(quads, q0 + per);
+    int above = 0;
+    if (e < E) {
+      const int key = key_s[e];
+      const int4* k4 = reinterpret_cast<const int4*>(key_s);
+      for (int i = q0; i < q1; ++i) {
+        const int4 k = k4[i];
+        above += (k.x > key) + (k.y > key) + (k.z > key) + (k.w > key);
+      }
+    }
+    above += __shfl_xor(above, 1);
+    if (R == 4) above += __shfl_xor(above, 2);
+    if (e < E && q % R == 0) usc[e] = above;
+  } else {
     const int lane = tid;
     int c[4], f[4], sc = 0, sf = 0;
 #pragma unroll
@@ -79,16 +113,12 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
         jf += nf;
       }
     }
-    int bc = ic - sc, bf = jf - sf;
+    int bc = ic - sc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = lane * 4 + i;
-      if (e < E) {
-        off[e] = bc;
-        usc[e] = bf;
-      }
+      if (e < E) off[e] = bc;
       bc += c[i];
-      bf += f[i];
     }
     if (lane == kWave - 1) {
       total_pairs = ic;

@@ -32,9 +32,17 @@
 // * The grid is sized from E (and T) alone; a workgroup reads the union size
 //   on the device and returns at once if it has no item, so inactive experts
 //   cost one scalar load and no host synchronisation is needed.
-// * Experts of the union are dealt to XCDs round-robin (the dispatcher deals
-//   workgroups round-robin over the 8 XCDs), so all of an expert's
-//   workgroups share one L2 for its activations and weights.
+// * Work is dealt to XCDs by hand (the dispatcher deals workgroups
+//   round-robin over the 8 XCDs, so workgroup b runs on XCD b % 8), in the
+//   union's order, which moe_bucket makes the dispatch order: buckets with
+//   more 16-token tiles first, equal ones by ascending id.  With at most 64
+//   tokens an expert, the union's experts go round-robin, all of an
+//   expert's bands on one XCD (sharing its L2 for the expert's
+//   activations).  With more, bucket sizes are skewed, and the union's
+//   (expert, band) units go round-robin instead, so every XCD gets an equal
+//   share of every expert; a band's token groups stay on one XCD, next to
+//   each other, so their shared weight reads meet in its L2.  Either way an
+//   XCD runs its largest buckets first.
 // * Weights come in one of two formats (a template parameter): bf16, or
 //   MXFP4 (FP4 E2M1 codes with one E8M0 scale per 32 values along the
 //   reduction axis, the format the paper serves GPT-OSS-120B in), whose
@@ -69,7 +77,6 @@ namespace eldr {
 #endif
 constexpr int kKStep = 32;        // k per MFMA
 constexpr int kFragElems = 512;   // bf16 values in one packed 16 x 32 weight fragment (1 KB)
-constexpr int kMaxExpertsPerXcd = (MOE_MAX_E + kNumXcd - 1) / kNumXcd;
 
 // Weight formats.
 //   kBf16:  packed by moe_pack_up_weights / moe_pack_down_weights; a ring
@@ -177,8 +184,6 @@ struct FfnArgs {
   int rows;                    // output rows per expert: up I, down H
   int kdim;                    // reduction length: up H, down I
   int tiles;                   // row bands per expert
-  int extra_groups;            // MULTI: slots per XCD beyond one group per expert, in bands
-  int max_groups;              // MULTI: token groups of the largest possible bucket (T)
   int experts;                 // E
   const u32x4* qcodes;         // MXFP4: packed FP4 codes (up: W1 and W3; down: W2)
   const uint32_t* qscales;     // MXFP4: packed E8M0 scales
@@ -254,6 +259,19 @@ __device__ __forceinline__ u32x4 expand_fp4(uint32_t w, uint32_t sc) {
 // from fp32 and splits it on the way into LDS; its epilogue writes h already
 // split, so the down kernel stages h with a plain copy.
 
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of 16
+// lanes (lanes shifted in from outside the row read 0), then the totals of
+// rows 0 and 2 broadcast into rows 1 and 3, then that of rows 0-1 into 2-3.
+__device__ __forceinline__ int wave_inclusive_sum(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 template <int MODE, int NT, bool MULTI, int FMT>
 __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs a) {
   constexpr int kFfnThreads = ffn_threads<MODE, FMT>();
@@ -271,16 +289,16 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
   const int lane = tid % kWave;
 
   // ---- work items -----------------------------------------------------------
-  // Expert u of the union belongs to XCD u % 8 (workgroups are dealt to the
-  // XCDs round-robin, so workgroup b runs on XCD b % 8 and is that XCD's
-  // slot b / 8).  An item is (expert, row band, token group of up to
-  // kGroupTokens tokens); an XCD's items are numbered expert by expert, and
-  // within an expert band by band with the band's token groups adjacent, so
-  // the workgroups that read one band's weights for different tokens run
-  // side by side and share the XCD's L2.  A slot takes items slot,
-  // slot + slots, ... .  Without MULTI (batches of at most kGroupTokens
-  // tokens) every expert has one group; with it, the group counts of this
-  // XCD's experts are read and prefix-summed first.
+  // Workgroups are dealt to the XCDs round-robin, so workgroup b runs on XCD
+  // b % 8 and is that XCD's slot b / 8.  An item is (expert, row band, token
+  // group of up to kGroupTokens tokens); an XCD's items are numbered expert
+  // by expert, and within an expert band by band with the band's token
+  // groups adjacent, so the workgroups that read one band's weights for
+  // different tokens run side by side and share the XCD's L2.  A slot takes
+  // items slot, slot + slots, ... .  Without MULTI (batches of at most
+  // kGroupTokens tokens) every expert has one group and the expert at union
+  // position u belongs to XCD u % 8; with it, the union's (expert, band)
+  // units are dealt round-robin.
   const int xcd = blockIdx.x % kNumXcd;
   const int slot = blockIdx.x / kNumXcd;
   const int slots = gridDim.x / kNumXcd;
@@ -583,51 +601,84 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     const int c = a.offsets[e + 1] - s_begin;
     if (c > 0) run_item(Int<0>{}, e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
   } else {
-    // Every wave builds the table of its XCD's experts in registers: lane m
-    // holds expert m's id (union_ids is read together with union_size; it is
-    // -1 past the union), bucket start and size, and its number of token
-    // groups.  An item is found with one ballot, and its expert's data with
-    // lane reads.
-    const int u_lane = xcd + kNumXcd * lane;
-    int e_lane = -1;
-    if (lane < kMaxExpertsPerXcd && u_lane < a.experts) e_lane = a.union_ids[u_lane];
-    const int U = *a.union_size;
-    if (U <= xcd) return;  // no expert on this XCD; also covers U < 0 (invalid routing)
-    const int M = (U - xcd + kNumXcd - 1) / kNumXcd;  // experts on this XCD
-    // An expert has at most max_groups token groups: slots past that bound
-    // leave before reading any bucket.
-    if (slot >= M * a.tiles * a.max_groups) return;
-    const bool member = lane < M && e_lane >= 0 && e_lane < a.experts;
-    int sb_lane = 0, c_lane = 0;
-    if (member) {
-      sb_lane = a.offsets[e_lane];
-      c_lane = a.offsets[e_lane + 1] - sb_lane;
+    // The union lists its experts in dispatch order (moe_bucket: more
+    // 16-token tiles first).  A projection's units are (expert, row band) pairs in
+    // that order, band by band: unit tiles * u + t is band t of the expert at
+    // union position u, and unit k goes to XCD k % 8.  So every XCD gets an
+    // equal share of every expert's bands (exactly equal when the band count
+    // is a multiple of 8, within one band otherwise) and the XCDs' loads match
+    // however skewed the buckets are; an XCD's items follow the union order,
+    // so the largest buckets start first; and an expert's items there are its
+    // bands in order with each band's token groups adjacent, reading the same
+    // weights side by side through the XCD's L2.
+    //
+    // Every wave holds the whole union, four positions a lane (4 * lane + j;
+    // union_ids is -1 past the union and is read together with union_size):
+    // id, bucket start and size, and the first item and number of items of
+    // the expert on this XCD.  Loads are issued unconditionally (from clamped
+    // indices), so the wave waits for two round trips rather than one a slot.
+    static_assert(MOE_MAX_E <= 4 * kWave, "four union positions a lane");
+    int e_j[4], sb_j[4], hi_j[4], c_j[4], n_j[4], first_j[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e_j[j] = a.union_ids[min(4 * lane + j, a.experts - 1)];
+    const int U = *a.union_size;  // U <= 0 (empty or invalid routing): no items
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int ec = e_j[j] >= 0 && e_j[j] < a.experts ? e_j[j] : 0;
+      sb_j[j] = a.offsets[ec];
+      hi_j[j] = a.offsets[ec + 1];
     }
-    const int g_lane = member ? (c_lane + kGroupTokens - 1) / kGroupTokens : 0;
-    // Items are ordered heaviest expert first (more tokens first, ties by
-    // union position), so the longest items start earliest: `before` is the
-    // number of token groups of the experts that precede this lane's.
-    int before = 0, total = 0;
-    for (int q = 0; q < M; ++q) {
-      const int cq = __builtin_amdgcn_readlane(c_lane, q);
-      const int gq = __builtin_amdgcn_readlane(g_lane, q);
-      if (cq > c_lane || (cq == c_lane && q < lane)) before += gq;
-      total += gq;
+    // (keeps the compiler from sinking a load into the branch that uses it)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(sb_j[j]), "+v"(hi_j[j]));
+    int lane_n = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int u = 4 * lane + j;
+      const bool member = u < min(U, a.experts) && e_j[j] >= 0 && e_j[j] < a.experts;
+      c_j[j] = member ? max(hi_j[j] - sb_j[j], 0) : 0;
+      const int g = (c_j[j] + kGroupTokens - 1) / kGroupTokens;
+      const int band0 = (xcd - a.tiles * u) & (kNumXcd - 1);  // first band on this XCD
+      const int nb = band0 < a.tiles ? (a.tiles - 1 - band0) / kNumXcd + 1 : 0;
+      n_j[j] = nb * g;
+      first_j[j] = lane_n;
+      lane_n += n_j[j];
     }
-    const int items = total * a.tiles;
-    for (int item = slot; item < items; item += slots) {
-      // the expert whose items cover this one
-      const int m = __ffsll((unsigned long long)__ballot(
-                        member && before * a.tiles <= item && item < (before + g_lane) * a.tiles)) - 1;
-      const int g = __builtin_amdgcn_readlane(g_lane, m);
-      const int r = item - __builtin_amdgcn_readlane(before, m) * a.tiles;
-      const int tile = r / g;
-      const int group = r - tile * g;
+    const int incl = wave_inclusive_sum(lane_n);
+    const int total = __builtin_amdgcn_readlane(incl, kWave - 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) first_j[j] += incl - lane_n;
+    for (int item = slot; item < total; item += slots) {
+      // the union position whose items cover this one
+      int js = -1, ls = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const unsigned long long hit =
+            __ballot(n_j[j] > 0 && first_j[j] <= item && item < first_j[j] + n_j[j]);
+        if (hit != 0) {
+          js = j;
+          ls = __ffsll(hit) - 1;
+        }
+      }
+      if (js < 0) break;  // not reached: the ranges cover [0, total)
+      auto pick = [&](const int (&v)[4]) {
+        int r = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (j == js) r = __builtin_amdgcn_readlane(v[j], ls);
+        return r;
+      };
+      const int cu = pick(c_j);
+      const int g = (cu + kGroupTokens - 1) / kGroupTokens;
+      const int r = item - pick(first_j);
+      const int band = r / g;
+      const int group = r - band * g;
+      const int tile = ((xcd - a.tiles * (4 * ls + js)) & (kNumXcd - 1)) + kNumXcd * band;
       const int p0 = group * kGroupTokens;
-      const int c = min(kGroupTokens, __builtin_amdgcn_readlane(c_lane, m) - p0);
+      const int c = min(kGroupTokens, cu - p0);
       if (c > 0) {
-        const int ie = __builtin_amdgcn_readlane(e_lane, m);
-        const int isb = __builtin_amdgcn_readlane(sb_lane, m);
+        const int ie = pick(e_j);
+        const int isb = pick(sb_j);
         if (g > 1)
           run_item(Int<1>{}, ie, tile, isb, p0, c);
         else
@@ -637,40 +688,50 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
   }
 }
 
-// Slots per XCD: one item per (expert, band) of the XCD's experts; batches
-// with more tokens than one item takes also get room for the average number
-// of extra token groups an XCD sees (T*K / (NT*16) extra groups at most in
-// all), and slots loop over any items beyond that.
+// Token tiles of 16 per item: enough for every bucket when T is small (a
+// bucket never exceeds T tokens), at most max_tiles.
+template <int FMT>
+static int ffn_nt(int T) {
+  int nt_T = T;
+#ifdef ELDR_FFN_FORCE_NT
+  nt_T = 16 * ELDR_FFN_FORCE_NT;
+#endif
+  return nt_T <= 16 ? 1 : nt_T <= 32 ? 2 : max_tiles<FMT>();
+}
+
+// Slots per XCD: one item per (expert, band) of an XCD's share of the
+// experts; batches with more tokens than one item takes also get room for an
+// XCD's share of the extra token groups (T*K / (NT*16) at most in all), and
+// slots loop over any items beyond that.
 template <int MODE, int FMT, int NT>
 static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
   const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
   if (T <= NT * 16) {
-    a.extra_groups = 0;
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, false, FMT>), dim3(kNumXcd * a.tiles * per_xcd),
                        dim3(ffn_threads<MODE, FMT>()), 0, s, a);
   } else {
     const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
-    a.extra_groups = extra;
-    a.max_groups = (T + NT * 16 - 1) / (NT * 16);
     hipLaunchKernelGGL((ffn_kernel<MODE, NT, true, FMT>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
                        dim3(ffn_threads<MODE, FMT>()), 0, s, a);
   }
 }
 
-// Token tiles of 16 per item: enough for every bucket when T is small (a
-// bucket never exceeds T tokens), at most max_tiles.
 template <int MODE, int FMT>
 static void launch_ffn_nt(const FfnArgs& a, int T, int K, int E, hipStream_t s) {
-  int nt_T = T;
-#ifdef ELDR_FFN_FORCE_NT
-  nt_T = 16 * ELDR_FFN_FORCE_NT;
-#endif
-  if (nt_T <= 16)
+  const int nt = ffn_nt<FMT>(T);
+  if (nt == 1)
     launch_ffn<MODE, FMT, 1>(a, T, K, E, s);
-  else if (nt_T <= 32)
+  else if (nt == 2)
     launch_ffn<MODE, FMT, 2>(a, T, K, E, s);
   else
     launch_ffn<MODE, FMT, max_tiles<FMT>()>(a, T, K, E, s);
+}
+
+// Row bands of a projection.
+template <int MODE, int FMT>
+static int ffn_tiles(const moe_dims& d) {
+  const int rows = MODE == kUp ? d.I : d.H;
+  return (rows + rows_per_block<MODE, FMT>() - 1) / rows_per_block<MODE, FMT>();
 }
 
 }  // namespace eldr
@@ -709,9 +770,8 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w13, const int3
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids,
-                   union_size, ws, d.I, d.H, 0, 0, 1, d.E, nullptr, nullptr};
-  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp, eldr::kBf16>() - 1) /
-             eldr::rows_per_block<eldr::kUp, eldr::kBf16>();
+                   union_size, ws, d.I, d.H, 0, d.E, nullptr, nullptr};
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kBf16>(d);
   eldr::launch_ffn_nt<eldr::kUp, eldr::kBf16>(up, d.T, d.K, d.E, s);
   return launch_status();
 }
@@ -730,10 +790,8 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E, nullptr, nullptr};
-  down.tiles =
-      (d.H + eldr::rows_per_block<eldr::kDown, eldr::kBf16>() - 1) /
-      eldr::rows_per_block<eldr::kDown, eldr::kBf16>();
+                     union_ids, union_size, y_perm, d.H, d.I, 0, d.E, nullptr, nullptr};
+  down.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kBf16>(d);
   eldr::launch_ffn_nt<eldr::kDown, eldr::kBf16>(down, d.T, d.K, d.E,
                                                reinterpret_cast<hipStream_t>(stream));
   return launch_status();
@@ -791,13 +849,12 @@ extern "C" int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes,
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, offsets, perm_token,
-                   union_ids, union_size, ws, d.I, d.H, 0, 0, 1, d.E,
+                   union_ids, union_size, ws, d.I, d.H, 0, d.E,
                    reinterpret_cast<const eldr::u32x4*>(up_codes),
                    reinterpret_cast<const uint32_t*>(up_scales)};
-  up.tiles = (d.I + eldr::rows_per_block<eldr::kUp, eldr::kMxfp4>() - 1) /
-             eldr::rows_per_block<eldr::kUp, eldr::kMxfp4>();
-  eldr::launch_ffn_nt<eldr::kUp, eldr::kMxfp4>(up, d.T, d.K, d.E,
-                                              reinterpret_cast<hipStream_t>(stream));
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kMxfp4>(d);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  eldr::launch_ffn_nt<eldr::kUp, eldr::kMxfp4>(up, d.T, d.K, d.E, s);
   return launch_status();
 }
 
@@ -817,12 +874,10 @@ extern "C" int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_cod
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), nullptr, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0, 0, 1, d.E,
+                     union_ids, union_size, y_perm, d.H, d.I, 0, d.E,
                      reinterpret_cast<const eldr::u32x4*>(down_codes),
                      reinterpret_cast<const uint32_t*>(down_scales)};
-  down.tiles =
-      (d.H + eldr::rows_per_block<eldr::kDown, eldr::kMxfp4>() - 1) /
-      eldr::rows_per_block<eldr::kDown, eldr::kMxfp4>();
+  down.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kMxfp4>(d);
   eldr::launch_ffn_nt<eldr::kDown, eldr::kMxfp4>(down, d.T, d.K, d.E,
                                                 reinterpret_cast<hipStream_t>(stream));
   return launch_status();
