@@ -108,11 +108,12 @@ int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, float* logits
  *   perm_token [T*K]   token of each slot: experts ascending, and within an
  *                      expert tokens ascending
  *   pair_pos   [T*K]   pair_pos[t*K + j] = slot of (t, topk_ids[t, j])
- *   union_ids  [E]     experts with counts > 0 in dispatch order -- more
- *                      16-token tiles (ceil(count / 16)) first, equal ones by
- *                      ascending id -- then -1 padding (moe_expert_ffn runs
- *                      the largest buckets first and deals experts to XCDs
- *                      in this order)
+ *   union_ids  [2E]    the union twice: [0, E) the experts with counts > 0
+ *                      ascending, then -1 padding; [E, 2E) the same experts
+ *                      in dispatch order -- more 16-token tiles
+ *                      (ceil(count / 16)) first, equal ones by ascending id --
+ *                      then -1 padding (moe_expert_ffn runs the largest
+ *                      buckets first and deals experts to XCDs in this order)
  *   union_size [1]     number of distinct experts U (stays on the device)
  * If an id is out of range or repeated within a token, union_size is set to
  * -1 and the other outputs are unspecified; moe_expert_ffn then does nothing.
@@ -177,7 +178,8 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * x [T, H] fp32; w13 (W1 and W3, [E, I, H] each) packed by
  * moe_pack_up_weights and w2 ([E, H, I]) packed by moe_pack_down_weights;
  * offsets [E+1],
- * perm_token [T*K], union_ids [E], union_size [1] int32 (moe_bucket output).
+ * perm_token [T*K], union_ids [2E], union_size [1] int32 (moe_bucket output;
+ * the FFN reads the dispatch-order half of union_ids).
  * y_perm [T*K, H] fp32 output (rows of slots whose expert is not in the
  * union are not written).  ws: device workspace of at least
  * moe_ffn_workspace_bytes(d) bytes, 16-byte aligned, contents irrelevant.

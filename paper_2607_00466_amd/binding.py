@@ -165,7 +165,7 @@ def moe_bucket(topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos, unio
     _need(offsets, "offsets", torch.int32, d.E + 1)
     _need(perm_token, "perm_token", torch.int32, d.T * d.K)
     _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
-    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_ids, "union_ids", torch.int32, 2 * d.E)
     _need(union_size, "union_size", torch.int32, 1)
     _check("moe_bucket", load().moe_bucket(_ptr(topk_ids), d, _ptr(counts), _ptr(offsets),
                                            _ptr(perm_token), _ptr(pair_pos), _ptr(union_ids),
@@ -184,7 +184,7 @@ def moe_expert_ffn(x, w13, w2, offsets, perm_token, union_ids, union_size, d: Mo
     _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
     _need(offsets, "offsets", torch.int32, d.E + 1)
     _need(perm_token, "perm_token", torch.int32, d.T * d.K)
-    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_ids, "union_ids", torch.int32, 2 * d.E)
     _need(union_size, "union_size", torch.int32, 1)
     _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
     ws_bytes = _need_ws(ws, d)
@@ -313,7 +313,7 @@ def _need_mx_down(down, d: MoeDims) -> None:
 def _need_routing(offsets, perm_token, union_ids, union_size, d: MoeDims) -> None:
     _need(offsets, "offsets", torch.int32, d.E + 1)
     _need(perm_token, "perm_token", torch.int32, d.T * d.K)
-    _need(union_ids, "union_ids", torch.int32, d.E)
+    _need(union_ids, "union_ids", torch.int32, 2 * d.E)
     _need(union_size, "union_size", torch.int32, 1)
 
 
@@ -394,7 +394,7 @@ class LayerBuffers:
             offsets=torch.empty(d.E + 1, **i32),
             perm_token=torch.empty(max(1, d.T * d.K), **i32),
             pair_pos=torch.empty(max(1, d.T * d.K), **i32),
-            union_ids=torch.empty(d.E, **i32),
+            union_ids=torch.empty(2 * d.E, **i32),
             union_size=torch.empty(1, **i32),
             y_perm=torch.empty((max(1, d.T * d.K), d.H), **f32),
             ws=torch.empty(max(16, nbytes) // 4, **f32),

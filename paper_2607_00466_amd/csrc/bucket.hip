@@ -5,11 +5,11 @@
 // it).  A slot's rank inside its bucket is the number of set bits below t,
 // so buckets list their tokens in ascending order without any sort, and the
 // result does not depend on the order in which threads ran.  The union is
-// listed in dispatch order: experts with more 16-token tiles (the expert
-// FFN's unit of work per item) first, equal ones by ascending id, so the FFN
-// starts its longest items first while batches of small buckets stream the
-// experts in address order.  An expert's position is the number of experts
-// with a larger (tiles, -id) key.
+// listed twice: in ascending id, then in dispatch order -- experts with more
+// 16-token tiles (the expert FFN's unit of work per item) first, equal ones
+// by ascending id -- so the FFN starts its longest items first while batches
+// of small buckets stream the experts in address order.  An expert's
+// dispatch position is the number of experts with a larger (tiles, -id) key.
 #include "common.hpp"
 
 namespace eldr {
@@ -34,7 +34,8 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
   uint16_t* pre = reinterpret_cast<uint16_t*>(mask + EW);         // [E][W] bits before word w
   int32_t* cnt = reinterpret_cast<int32_t*>(pre + ((EW + 1) & ~1));  // [E]
   int32_t* off = cnt + E;                                         // [E]
-  int32_t* usc = off + E;                                         // [E] union position
+  int32_t* usc = off + E;                                         // [E] position, ascending union
+  int32_t* rnk = usc + E;                                         // [E] position, dispatch order
   const int tid = threadIdx.x;
   const int P = T * K;
 
@@ -91,7 +92,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
     }
     above += __shfl_xor(above, 1);
     if (R == 4) above += __shfl_xor(above, 2);
-    if (e < E && q % R == 0) usc[e] = above;
+    if (e < E && q % R == 0) rnk[e] = above;
   } else {
     const int lane = tid;
     int c[4], f[4], sc = 0, sf = 0;
@@ -113,12 +114,16 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
         jf += nf;
       }
     }
-    int bc = ic - sc;
+    int bc = ic - sc, bf = jf - sf;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = lane * 4 + i;
-      if (e < E) off[e] = bc;
+      if (e < E) {
+        off[e] = bc;
+        usc[e] = bf;
+      }
       bc += c[i];
+      bf += f[i];
     }
     if (lane == kWave - 1) {
       total_pairs = ic;
@@ -143,10 +148,16 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
   for (int e = tid; e < E; e += kBucketThreads) {
     counts[e] = cnt[e];
     offsets[e] = off[e];
-    if (cnt[e] > 0) union_ids[usc[e]] = e;
+    if (cnt[e] > 0) {
+      union_ids[usc[e]] = e;
+      union_ids[E + rnk[e]] = e;
+    }
   }
   for (int u = tid; u < E; u += kBucketThreads)
-    if (u >= U) union_ids[u] = -1;
+    if (u >= U) {
+      union_ids[u] = -1;
+      union_ids[E + u] = -1;
+    }
   if (tid == 0) {
     offsets[E] = total_pairs;
     *union_size = ok ? U : -1;
@@ -156,7 +167,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(
 size_t bucket_lds_bytes(int T, int E) {
   const size_t W = (size_t)(T + 31) / 32;
   const size_t EW = (size_t)E * W;
-  return EW * 4 + ((EW + 1) & ~(size_t)1) * 2 + (size_t)E * 3 * 4;
+  return EW * 4 + ((EW + 1) & ~(size_t)1) * 2 + (size_t)E * 4 * 4;
 }
 
 }  // namespace eldr

@@ -178,7 +178,7 @@ struct FfnArgs {
   const uint16_t* wa;          // bf16, packed by band: up W1 and W3; down W2
   const int32_t* offsets;      // [E+1]
   const int32_t* perm_token;   // [T*K]
-  const int32_t* union_ids;    // [E]
+  const int32_t* union_ids;    // [E]: the union in dispatch order (moe_bucket's second half)
   const int32_t* union_size;   // [1]
   void* dst;                   // up: h [T*K, I] as bf16 pairs; down: y_perm [T*K, H] fp32
   int rows;                    // output rows per expert: up I, down H
@@ -769,7 +769,7 @@ extern "C" int moe_expert_ffn_up(const float* x, const uint16_t* w13, const int3
   if (!aligned16(x) || !aligned16(w13) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids,
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids + d.E,
                    union_size, ws, d.I, d.H, 0, d.E, nullptr, nullptr};
   up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kBf16>(d);
   eldr::launch_ffn_nt<eldr::kUp, eldr::kBf16>(up, d.T, d.K, d.E, s);
@@ -790,7 +790,7 @@ extern "C" int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int
   if (!aligned16(ws) || !aligned16(w2) || !aligned16(y_perm)) return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), w2, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0, d.E, nullptr, nullptr};
+                     union_ids + d.E, union_size, y_perm, d.H, d.I, 0, d.E, nullptr, nullptr};
   down.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kBf16>(d);
   eldr::launch_ffn_nt<eldr::kDown, eldr::kBf16>(down, d.T, d.K, d.E,
                                                reinterpret_cast<hipStream_t>(stream));
@@ -849,7 +849,7 @@ extern "C" int moe_expert_ffn_mxfp4_up(const float* x, const uint8_t* up_codes,
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, offsets, perm_token,
-                   union_ids, union_size, ws, d.I, d.H, 0, d.E,
+                   union_ids + d.E, union_size, ws, d.I, d.H, 0, d.E,
                    reinterpret_cast<const eldr::u32x4*>(up_codes),
                    reinterpret_cast<const uint32_t*>(up_scales)};
   up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kMxfp4>(d);
@@ -874,7 +874,7 @@ extern "C" int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_cod
     return MOE_ERR_UNSUPPORTED;
   if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
   eldr::FfnArgs down{reinterpret_cast<const uint4*>(ws), nullptr, offsets, perm_token,
-                     union_ids, union_size, y_perm, d.H, d.I, 0, d.E,
+                     union_ids + d.E, union_size, y_perm, d.H, d.I, 0, d.E,
                      reinterpret_cast<const eldr::u32x4*>(down_codes),
                      reinterpret_cast<const uint32_t*>(down_scales)};
   down.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kMxfp4>(d);

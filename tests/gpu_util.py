@@ -95,12 +95,14 @@ def compare_buckets(g: dict, ids: np.ndarray, E: int) -> None:
     assert np.array_equal(g["pair_pos"], r["pair_pos"]), "pair_pos"
     assert g["union_size"] == r["union_size"]
     U = r["union_size"]
-    # the union is a set (the oracle lists it ascending); the library lists it
-    # in dispatch order, more 16-token tiles first and equal ones by ascending
-    # id, an order the oracle's counts fix
+    E_ = len(r["counts"])
+    assert np.array_equal(g["union_ids"][:U], r["union_ids"]), "union_ids"
+    assert np.all(g["union_ids"][U:E_] == -1)
+    # then the same experts in dispatch order: more 16-token tiles first, equal
+    # ones by ascending id, an order the oracle's counts fix
     order = sorted(r["union_ids"].tolist(), key=lambda e: (-((int(r["counts"][e]) + 15) // 16), e))
-    assert g["union_ids"][:U].tolist() == order, "union_ids"
-    assert np.all(g["union_ids"][U:] == -1)
+    assert g["union_ids"][E_:E_ + U].tolist() == order, "union_ids dispatch order"
+    assert np.all(g["union_ids"][E_ + U:] == -1)
 
 
 def output_errors(gpu: np.ndarray, ref: np.ndarray) -> tuple[float, float]:

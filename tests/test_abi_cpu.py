@@ -27,7 +27,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_status_strings(lib):
-    assert lib.moe_abi_version() == 1
+    assert lib.moe_abi_version() == 2
     for st in (B.MOE_OK, B.MOE_ERR_INVALID, B.MOE_ERR_UNSUPPORTED, B.MOE_ERR_WORKSPACE, B.MOE_ERR_HIP):
         assert B.status_string(st).startswith("MOE_")
     assert B.status_string(12345) == "unknown status"
