@@ -121,6 +121,41 @@ def test_heavy_experts_on_one_xcd():
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
+@pytest.mark.parametrize("T", [64, 100])
+def test_most_experts(T):
+    # E = 256, the most the library takes: the union reaches the last of the
+    # four union positions a lane holds in the FFN's lookup.  T = 64 deals
+    # whole experts over the XCDs, T = 100 deals (expert, band) units.
+    G.say(f"case: E=256 top-8 H=256 I=128 T={T}, gate-routed")
+    shape = synth.LayerShape("most_experts", E=256, K=8, H=256, I=128)
+    layer = G.Layer(shape, T, seed=30 + T)
+    g = layer.run()
+    assert g["union_size"] > 192
+    _full_check(layer, g, True)
+
+
+def test_most_experts_heavy_buckets():
+    # E = 256 with experts 250..253 in every token (three token groups each,
+    # first in dispatch order) beside an almost full union of light experts.
+    shape = synth.LayerShape("most_experts_heavy", E=256, K=8, H=256, I=128)
+    T = 200
+    G.say(f"case: E=256 top-8 H=256 I=128 T={T}, experts 250..253 take every token")
+    rng = np.random.default_rng(13)
+    heavy = np.array([250, 251, 252, 253], np.int32)
+    light = np.setdiff1d(np.arange(256, dtype=np.int32), heavy)
+    ids = np.empty((T, 8), np.int32)
+    for t in range(T):
+        ids[t, :4] = heavy
+        ids[t, 4:] = rng.choice(light, 4, replace=False)
+    w = rng.dirichlet(np.ones(8), size=T).astype(np.float32)
+    layer = G.Layer(shape, T, seed=14)
+    g = layer.run(routing=(ids, w))
+    assert g["union_size"] > 192
+    assert g["counts"][heavy].tolist() == [T] * 4
+    assert g["union_ids"][256:260].tolist() == heavy.tolist()  # first in dispatch order
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
 def test_ragged_shape_partial_bands():
     # H and I multiples of 32 but not of the 64/128-row bands; E not a multiple of 8.
     G.say("case: ragged shape E=13 top-3 H=352 I=96 T=21")
