@@ -203,6 +203,7 @@ def moe_expert_ffn_up(x, w13, offsets, perm_token, union_ids, union_size, d: Moe
                       stream=None) -> None:
     _need(x, "x", torch.float32, d.T * d.H)
     _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
     ws_bytes = _need_ws(ws, d)
     _check("moe_expert_ffn_up", load().moe_expert_ffn_up(
         _ptr(x), _ptr(w13), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
@@ -213,6 +214,7 @@ def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: M
                         stream=None) -> None:
     _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
     _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
     ws_bytes = _need_ws(ws, d)
     _check("moe_expert_ffn_down", load().moe_expert_ffn_down(
         _ptr(ws), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids), _ptr(union_size), d,
