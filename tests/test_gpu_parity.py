@@ -251,6 +251,29 @@ def test_bucket_large_batch():
     G.compare_buckets(G.fetch(buf, d), ids.astype(np.int64), E)
 
 
+def test_union_dispatch_order_at_tile_boundaries():
+    # One pick per token, so each expert's count is set exactly: 15, 16 and 17
+    # tokens straddle the first 16-token tile, 32/33 the second, 48/49 the
+    # third; experts 6 and 11 take none.  Dispatch order: more tiles first,
+    # equal tiles by ascending id.
+    E = 12
+    counts = [15, 16, 17, 32, 33, 1, 0, 16, 48, 49, 2, 0]
+    ids = np.repeat(np.arange(E, dtype=np.int32), counts)
+    np.random.default_rng(8).shuffle(ids)
+    T = ids.size
+    G.say(f"case: bucket only, T={T} E={E} K=1, counts {counts}")
+    d = B.dims(T, 64, E, 1, 32)
+    buf = B.LayerBuffers.allocate(d)
+    B.moe_bucket(torch.from_numpy(ids.reshape(T, 1)).cuda(), d, buf.counts, buf.offsets,
+                 buf.perm_token, buf.pair_pos, buf.union_ids, buf.union_size)
+    torch.cuda.synchronize()
+    g = G.fetch(buf, d)
+    assert g["union_size"] == 10
+    assert g["union_ids"][:E].tolist() == [0, 1, 2, 3, 4, 5, 7, 8, 9, 10, -1, -1]
+    assert g["union_ids"][E:].tolist() == [9, 4, 8, 2, 3, 0, 1, 5, 7, 10, -1, -1]
+    G.compare_buckets(g, ids.reshape(T, 1).astype(np.int64), E)
+
+
 def test_combine_alone():
     G.say("case: combine on oracle slot outputs, qwen shape T=64")
     T, E, K, H = 64, 128, 8, 2048
