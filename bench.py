@@ -270,8 +270,11 @@ def mxfp4_workload(path: str, steps: int, warmup: int, layers: int = 36,
         for fmt, cls in (("mxfp4", MxBench), ("bf16", Bench)):
             if fmt not in formats:
                 continue
+            log(f"gpt-oss {fmt}: building the layer (synthetic weights"
+                f"{', quantized to MXFP4' if fmt == 'mxfp4' else ''})")
             bench = cls(shape, T)
             for U in cases:
+                log(f"gpt-oss {fmt}: timing {'gate-routed' if U is None else f'controlled U={U}'}")
                 routing = None
                 if U is not None:
                     ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0)
