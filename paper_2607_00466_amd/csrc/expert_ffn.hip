@@ -602,9 +602,9 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     if (c > 0) run_item(Int<0>{}, e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
   } else {
     // The union lists its experts in dispatch order (moe_bucket: more
-    // 16-token tiles first).  A projection's units are (expert, row band) pairs in
-    // that order, band by band: unit tiles * u + t is band t of the expert at
-    // union position u, and unit k goes to XCD k % 8.  So every XCD gets an
+    // 16-token tiles first).  A projection's units are (expert, row band)
+    // pairs in that order, band by band: unit tiles * u + t is band t of the
+    // expert at union position u, and unit k goes to XCD k % 8.  So every XCD gets an
     // equal share of every expert's bands (exactly equal when the band count
     // is a multiple of 8, within one band otherwise) and the XCDs' loads match
     // however skewed the buckets are; an XCD's items follow the union order,
