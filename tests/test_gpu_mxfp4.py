@@ -126,7 +126,8 @@ def test_pack_mxfp4_is_the_documented_permutation(E, I, H):
     (8, 2, 192, 320, 8),      # one token tile; up: a lone tail chunk, down: a partial row band
     (8, 2, 192, 320, 24),     # two token tiles
     (6, 3, 256, 128, 100),    # buckets of about 50 tokens: four token tiles
-    (4, 2, 256, 128, 200),    # buckets of about 100 tokens: two token groups, the work plan
+    (4, 2, 256, 128, 200),    # buckets of about 100 tokens: two token groups
+    (256, 4, 128, 128, 100),  # the most experts: the union fills four positions a lane
     (4, 2, 2880, 2880, 40),   # full-size reductions: 11 whole chunks and a tail
 ])
 def test_mxfp4_layer_matches_oracle(E, K, H, I, T):
