@@ -741,8 +741,7 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
     packed.append(tuple(w.clone() for w in packed[0]))
     del raw
     wg = torch.from_numpy(synth.gate_weights(shape, 0, 0)).cuda()
-    results = {}
-    for name, assign in (("eldr", eldr_w), ("round_robin", rr_w)):
+    def measure(assign):
         unions = np.zeros((workers, L))
         sizes = np.bincount(assign, minlength=workers)
         for w in range(workers):
@@ -789,16 +788,28 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
             torch.cuda.synchronize()
             worker_us.append(e0.elapsed_time(e1) / 10 * 1e3)
             del g, buf
-        results[name] = {"mean_union": float(unions.mean()), "max_batch": int(sizes.max()),
-                         "min_batch": int(sizes.min()),
-                         "mean_worker_step_us": float(np.mean(worker_us)),
-                         "max_worker_step_us": float(np.max(worker_us))}
-    e, r = results["eldr"], results["round_robin"]
+        return {"mean_union": float(unions.mean()), "max_batch": int(sizes.max()),
+                "min_batch": int(sizes.min()),
+                "mean_worker_step_us": float(np.mean(worker_us)),
+                "max_worker_step_us": float(np.max(worker_us))}
+
+    e, r = measure(eldr_w), measure(rr_w)
+    # The band width tau trades locality (tau = 0: always the most similar
+    # worker) for balance (tau = 2: every worker is in the band, so the least
+    # loaded one is chosen).
+    sweep = []
+    for tau in (0.0, 0.02, 0.05, 0.1, 0.2, 2.0):
+        assign, _ = B.eldr_route_batch(S, C, np.zeros(workers, np.int32), tau)
+        m = measure(assign)
+        m["tau"] = tau
+        sweep.append(m)
+        log(f"routing tau {tau}: union {m['mean_union']:.1f}, batches {m['min_batch']}-{m['max_batch']}, "
+            f"worker step mean {m['mean_worker_step_us']:.0f} us, slowest {m['max_worker_step_us']:.0f} us")
     rec = {"workload": f"ELDR vs round-robin: {workers} workers x {per_worker} requests, 8 synthetic domains, "
                        f"48 MoE layers (E=128, top-8); decode step timed on {layers_timed} Qwen3-30B-A3B-shaped layers",
            "fit_s": round(fit_s, 2), "n_star": n_star, "rho": round(float(curve[n_star - 1]), 4),
            "kmeans_iterations": iters, "route_us_per_request": round(route_us, 2),
-           "eldr": e, "round_robin": r,
+           "eldr": e, "round_robin": r, "tau_sweep": sweep,
            "union_reduction": round(1 - e["mean_union"] / r["mean_union"], 4),
            "mean_step_reduction": round(1 - e["mean_worker_step_us"] / r["mean_worker_step_us"], 4),
            "max_step_reduction": round(1 - e["max_worker_step_us"] / r["max_worker_step_us"], 4)}
