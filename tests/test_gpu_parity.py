@@ -238,6 +238,22 @@ def test_invalid_routing_flags_union():
     assert g["union_size"] == -1
 
 
+def test_invalid_routing_over_64_tokens():
+    # The same flag when the batch takes the kernels that deal (expert, band)
+    # units over the XCDs: they read no union entry and write nothing.
+    T = 100
+    G.say(f"case: repeated id within a token, T={T} -> union_size = -1, FFN does nothing")
+    layer = G.Layer(TINY, T)
+    rng = np.random.default_rng(21)
+    ids = np.stack([rng.choice(TINY.E, TINY.K, replace=False) for _ in range(T)]).astype(np.int32)
+    ids[57] = [9, 9]
+    w = np.full((T, TINY.K), 0.5, np.float32)
+    layer.buf.y_perm.fill_(123.0)
+    g = layer.run(routing=(ids, w))
+    assert g["union_size"] == -1
+    assert np.all(g["y_slots"] == 123.0)
+
+
 def test_bucket_large_batch():
     G.say("case: bucket only, T=4096 E=128 K=8 (bitmap limit)")
     T, E, K = 4096, 128, 8
