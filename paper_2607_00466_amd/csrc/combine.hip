@@ -5,7 +5,10 @@
 
 namespace eldr {
 
-constexpr int kCombineThreads = 256;
+// One wave per workgroup: at H = 2048 and T = 64 that is 512 workgroups, so
+// every CU shares the kernel's two dependent memory round trips (slot, then
+// row).  Measured about 4% shorter than 256-thread workgroups.
+constexpr int kCombineThreads = 64;
 
 // One workgroup row per token: the token's K slots and weights are the same
 // for every thread (scalar loads), and all K expert rows are requested before
