@@ -117,7 +117,9 @@ int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, float* logits
  *   union_size [1]     number of distinct experts U (stays on the device)
  * If an id is out of range or repeated within a token, union_size is set to
  * -1 and the other outputs are unspecified; moe_expert_ffn then does nothing.
- * Requires E * ceil(T / 32) <= 16384 (per-expert token bitmaps in LDS).
+ * Requires E * ceil(T / 32) <= 16384 (per-expert token bitmaps in LDS),
+ * else MOE_ERR_UNSUPPORTED; above 8192 it raises the kernel's dynamic LDS
+ * limit on the current device first (MOE_ERR_HIP if the runtime refuses).
  */
 int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* offsets,
                int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,

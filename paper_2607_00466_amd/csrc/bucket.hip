@@ -185,14 +185,14 @@ extern "C" int moe_bucket(const int32_t* topk_ids, moe_dims d, int32_t* counts, 
     return MOE_ERR_UNSUPPORTED;
   if ((long long)d.E * ((d.T + 31) / 32) > eldr::kBucketMaxWords) return MOE_ERR_UNSUPPORTED;
   const size_t lds = eldr::bucket_lds_bytes(d.T, d.E);
-  if (lds > 64 * 1024) {
-    static bool raised = false;
-    if (!raised) {
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(eldr::bucket_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
-      raised = true;
-    }
-  }
+  // Bitmaps above 64 KiB (E * ceil(T / 32) > 8192 words) need the kernel's
+  // dynamic LDS limit raised, on the current device, before the launch; the
+  // call is cheap and shapes that need it are prefill-sized, so it is made on
+  // every such call rather than cached.
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute(reinterpret_cast<const void*>(eldr::bucket_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return MOE_ERR_HIP;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(eldr::bucket_kernel, dim3(1), dim3(eldr::kBucketThreads), lds, s, topk_ids,
                      d.T, d.E, d.K, counts, offsets, perm_token, pair_pos, union_ids, union_size);
