@@ -306,6 +306,33 @@ def test_combine_alone():
     assert np.abs(out.cpu().numpy() - ref).max() <= 1e-5 * np.abs(ref).max()
 
 
+@pytest.mark.parametrize("T,K,H", [(3, 2, 32), (5, 4, 288), (7, 8, 2880)])
+def test_combine_ragged_rows_and_slots_out_of_range(T, K, H):
+    """Hidden sizes that leave the last wave partly idle (H/4 not a multiple of
+    64), and slots outside [0, T*K), which contribute nothing: the reference
+    points them at an appended zero row."""
+    G.say(f"case: combine alone, T={T} K={K} H={H}, some slots out of range")
+    rng = np.random.default_rng(T * 100 + H)
+    P = T * K
+    pp = rng.permutation(P).astype(np.int32).reshape(T, K)
+    pp[0, K - 1] = -1
+    pp[T - 1, 0] = P
+    pp[T // 2, K // 2] = 1 << 30
+    w = rng.random((T, K)).astype(np.float32)
+    y = rng.standard_normal((P, H)).astype(np.float32)
+    d = B.dims(T, H, max(K, 8), K, 32)
+    out = torch.full((T, H), float("nan"), device="cuda")
+    B.moe_combine(torch.from_numpy(y).cuda(), torch.from_numpy(pp.ravel()).cuda(),
+                  torch.from_numpy(w).cuda(), d, out)
+    torch.cuda.synchronize()
+    y_ext = np.vstack([y.astype(np.float64), np.zeros((1, H))])
+    pp_ref = np.where((pp >= 0) & (pp < P), pp, P)
+    ref = O.combine(y_ext, pp_ref, w.astype(np.float64))
+    got = out.cpu().numpy()
+    assert np.isfinite(got).all()
+    assert np.abs(got - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
 def test_deterministic(qwen_layer):
     G.say("case: two runs of the qwen layer are bitwise equal")
     a = qwen_layer.run()
