@@ -254,10 +254,13 @@ def test_invalid_routing_over_64_tokens():
     assert np.all(g["y_slots"] == 123.0)
 
 
-def test_bucket_large_batch():
-    G.say("case: bucket only, T=4096 E=128 K=8 (bitmap limit)")
-    T, E, K = 4096, 128, 8
-    rng = np.random.default_rng(5)
+@pytest.mark.parametrize("T,E", [(4096, 128), (2048, 256)])
+def test_bucket_large_batch(T, E):
+    # Both fill the 16384-word bitmap limit (LDS above 64 KiB); E = 256 also
+    # ranks each expert with two threads instead of four.
+    G.say(f"case: bucket only, T={T} E={E} K=8 (bitmap limit)")
+    K = 8
+    rng = np.random.default_rng(5 + E)
     ids = np.stack([rng.choice(E, K, replace=False) for _ in range(T)]).astype(np.int32)
     d = B.dims(T, 64, E, K, 32)
     buf = B.LayerBuffers.allocate(d)
