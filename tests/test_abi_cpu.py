@@ -103,6 +103,14 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.moe_combine(None, None, None, d, None, None) == B.MOE_OK
 
 
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    # No CPU fallback: without the built HIP library every call path raises.
+    monkeypatch.setattr(B, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        B.load(str(tmp_path / "libeldr_moe.so"))
+    assert B._lib is None
+
+
 def test_binding_requires_device_tensors():
     import torch
     d = B.dims(2, 64, 4, 2, 32)
