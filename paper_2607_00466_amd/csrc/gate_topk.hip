@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kSelectThreads) void gate_select_kernel(
     ids[(size_t)(t0 + t) * K + rank] = e;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nt * K; i += kSelectThreads) {
+  for (int i = threadIdx.x; i < nt * K; i += blockDim.x) {
     const int tt = i / K;
     const int j = i - tt * K;
     float sum = 0.0f;
@@ -203,12 +203,15 @@ extern "C" int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, fl
                      logits);
   st = launch_status();
   if (st != MOE_OK) return st;
-  // As many tokens per workgroup as give every thread one (token, expert)
-  // pair (E <= 256, so at least one token).
-  const int tpb = eldr::kSelectThreads / d.E;
+  // One token per workgroup, one (token, expert) pair per thread, E rounded
+  // up to whole waves (E <= 256 = kSelectThreads): decode batches then spread
+  // the rank loops' LDS reads over T CUs.  Measured about 2% shorter than
+  // packing 256 / E tokens into 256 threads.
+  const int tpb = 1;
+  const int sel_threads = (d.E + eldr::kWave - 1) / eldr::kWave * eldr::kWave;
   const size_t lds = (size_t)tpb * (((d.E + 1) & ~1) * sizeof(uint64_t) + MOE_MAX_K * sizeof(float));
   dim3 g2((d.T + tpb - 1) / tpb);
-  hipLaunchKernelGGL(eldr::gate_select_kernel, g2, dim3(eldr::kSelectThreads), lds, s, logits, d.T,
+  hipLaunchKernelGGL(eldr::gate_select_kernel, g2, dim3(sel_threads), lds, s, logits, d.T,
                      d.E, d.K, tpb, topk_ids, topk_w);
   return launch_status();
 }
