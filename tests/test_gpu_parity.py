@@ -182,6 +182,20 @@ def test_k_equals_e():
     _full_check(layer, g, True)
 
 
+@pytest.mark.parametrize("T", [5, 70])
+def test_single_expert(T):
+    # E = K = 1: every token on expert 0 with weight 1, a union of one.  T = 70
+    # gives that expert two token groups (the (expert, band) dealing).
+    G.say(f"case: E=1 top-1 H=256 I=128 T={T}, gate-routed")
+    shape = synth.LayerShape("single_expert", E=1, K=1, H=256, I=128)
+    layer = G.Layer(shape, T, seed=40 + T)
+    g = layer.run()
+    assert g["union_size"] == 1
+    assert g["counts"].tolist() == [T]
+    assert np.all(g["weights"] == 1.0)
+    _full_check(layer, g, True)
+
+
 def test_duplicate_gate_rows_tie_to_lower_id():
     G.say("case: gate rows 3 and 11 identical (exact ties), tiny shape T=64")
     layer = G.Layer(TINY, 64, seed=9)
