@@ -286,8 +286,11 @@ int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_codes,
 
 /*
  * moe_combine -- weighted unpermute: out[t, :] = sum over j = 0..K-1 (in that
- * order) of topk_w[t, j] * y_perm[pair_pos[t*K + j], :].  Deterministic, no
- * atomics.  y_perm [T*K, H], topk_w [T, K] fp32, pair_pos [T*K] int32
+ * order) of topk_w[t, j] * y_perm[pair_pos[t*K + j], :].  This is the last
+ * step of the MoE layer: a token's output is its selected experts' outputs
+ * mixed by the gate's renormalised weights (Background, Mixture-of-Experts
+ * LLMs; standard top-k gating, which ELDR leaves unchanged: Related Work,
+ * "lossless").  Deterministic, no atomics.  y_perm [T*K, H], topk_w [T, K] fp32, pair_pos [T*K] int32
  * (inputs); out [T, H] fp32 (output).  A pair_pos entry outside [0, T*K)
  * contributes nothing.
  */

@@ -81,7 +81,10 @@ int eldr_balanced_kmeans(const float* S, int32_t N, int32_t d, int32_t K, const 
  * s_k = cos(s, centroids[k]) and s* = max_k s_k, among the workers with
  * s_k >= s* - tau pick the one with the fewest in-flight requests loads[k];
  * ties go to the higher s_k, then the lower k.  s [d], centroids [K, d],
- * loads [K].  *worker receives the choice.
+ * loads [K].  *worker receives the choice.  tau must be finite and >= 0
+ * (the paper sweeps it over [0, 1]), else MOE_ERR_INVALID.  A non-finite
+ * signature or centroid leaves no worker in the band: *worker = -1 and
+ * MOE_ERR_INVALID.
  */
 int eldr_route(const float* s, int32_t d, const float* centroids, int32_t K,
                const int32_t* loads, float tau, int32_t* worker);
@@ -89,7 +92,9 @@ int eldr_route(const float* s, int32_t d, const float* centroids, int32_t K,
 /*
  * eldr_route_batch -- route R requests in order with eldr_route, each choice
  * adding one in-flight request to its worker: S [R, d], loads [K] (in/out),
- * workers [R].
+ * workers [R].  Errors as eldr_route; routing stops at the first request with
+ * no worker, which and every later one get workers[r] = -1 and add no load
+ * (the requests before it stay routed).
  */
 int eldr_route_batch(const float* S, int32_t R, int32_t d, const float* centroids, int32_t K,
                      int32_t* loads, float tau, int32_t* workers);

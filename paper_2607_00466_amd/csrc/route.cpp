@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <limits>
 #include <numeric>
+#include <cmath>
 #include <vector>
 
 #include "eldr_route.h"
@@ -347,18 +348,31 @@ int route_one(const float* s, int32_t d, const float* centroids, int32_t K, cons
 
 }  // namespace
 
+// The band width is a non-negative finite number (the paper sweeps it over
+// [0, 1]); a negative or NaN tau could leave the band empty.
+static bool valid_tau(float tau) { return std::isfinite(tau) && tau >= 0.0f; }
+
 extern "C" int eldr_route(const float* s, int32_t d, const float* centroids, int32_t K,
                           const int32_t* loads, float tau, int32_t* worker) {
-  if (!s || !centroids || !loads || !worker || d <= 0 || K <= 0) return MOE_ERR_INVALID;
-  *worker = route_one(s, d, centroids, K, loads, tau);
-  return MOE_OK;
+  if (!s || !centroids || !loads || !worker || d <= 0 || K <= 0 || !valid_tau(tau))
+    return MOE_ERR_INVALID;
+  const int w = route_one(s, d, centroids, K, loads, tau);
+  *worker = w;
+  // no worker in the band: a similarity was NaN (a non-finite signature or centroid)
+  return w < 0 ? MOE_ERR_INVALID : MOE_OK;
 }
 
 extern "C" int eldr_route_batch(const float* S, int32_t R, int32_t d, const float* centroids,
                                 int32_t K, int32_t* loads, float tau, int32_t* workers) {
-  if (!S || !centroids || !loads || !workers || R < 0 || d <= 0 || K <= 0) return MOE_ERR_INVALID;
+  if (!S || !centroids || !loads || !workers || R < 0 || d <= 0 || K <= 0 || !valid_tau(tau))
+    return MOE_ERR_INVALID;
   for (int32_t r = 0; r < R; ++r) {
     const int w = route_one(S + (size_t)r * d, d, centroids, K, loads, tau);
+    if (w < 0) {
+      // stop at the first request that has no worker; it and the rest stay unrouted
+      for (int32_t q = r; q < R; ++q) workers[q] = -1;
+      return MOE_ERR_INVALID;
+    }
     workers[r] = w;
     loads[w] += 1;
   }

@@ -124,7 +124,7 @@ def test_pack_mxfp4_is_the_documented_permutation(E, I, H):
 
 @pytest.mark.parametrize("E,K,H,I,T", [
     (8, 2, 192, 320, 8),      # one token tile; up: a lone tail chunk, down: a partial row band
-    (8, 2, 192, 320, 24),     # two token tiles
+    (8, 2, 192, 320, 24),     # the two-tile kernel; buckets of about 6 take its one-tile pass
     (6, 3, 256, 128, 100),    # buckets of about 50 tokens: four token tiles
     (4, 2, 256, 128, 200),    # buckets of about 100 tokens: two token groups
     (256, 4, 128, 128, 100),  # the most experts: the union fills four positions a lane
@@ -134,6 +134,20 @@ def test_mxfp4_layer_matches_oracle(E, K, H, I, T):
     G.say(f"case: MXFP4 layer E={E} top-{K} H={H} I={I} T={T}, gate-routed")
     layer = MxLayer(synth.LayerShape("mx", E=E, K=K, H=H, I=I), T, seed=E + T)
     _check_layer(layer, layer.run())
+
+
+@pytest.mark.parametrize("T,heavy", [(24, [(2, 24), (5, 17)]),
+                                     (32, [(3, 17), (7, 24), (11, 32)])])
+def test_mxfp4_two_tile_pass(T, heavy):
+    # 16 < T <= 32 takes the two-tile kernel; buckets of 17, 24 and 32 tokens
+    # run its two-tile pass.  H = 640 is two full 8-step chunks and a tail.
+    sh = synth.LayerShape("mx_two_tile", E=16, K=4, H=640, I=320)
+    G.say(f"case: MXFP4 E=16 top-4 H=640 I=320 T={T}, buckets of {[n for _, n in heavy]} tokens")
+    ids, w = G.fixed_bucket_routing(T, sh.E, sh.K, heavy, seed=T + 1)
+    layer = MxLayer(sh, T, seed=T)
+    g = layer.run((ids, w))
+    assert [int(g["counts"][e]) for e, _ in heavy] == [n for _, n in heavy]
+    _check_layer(layer, g, (ids.astype(np.int64), w))
 
 
 def test_mxfp4_full_code_and_scale_range():

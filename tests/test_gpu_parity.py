@@ -44,9 +44,16 @@ def _full_check(layer: G.Layer, g: dict, routed_by_gate: bool, routing=None) -> 
     out = O.combine(y, b["pair_pos"], np.asarray(wts, np.float64))
     G.check_output(g["out"], out, "layer output (GPU routing)")
     if routed_by_gate:
-        ref = O.moe_layer(layer.x_np, layer.wg_np, w1, w3, w2, s.K)
         ok = ~near
-        G.check_output(g["out"][ok], ref["out"][ok], "layer output vs oracle end to end")
+        logits = O.gate_logits(layer.x_np, layer.wg_np)
+        ref_ids = O.select_experts(logits, s.K)
+        if np.array_equal(ref_ids, g["ids"]):
+            # the oracle routes exactly as the GPU did, so its slot outputs are
+            # the ones above; only the oracle's own weights remain to apply
+            ref_out = O.combine(y, b["pair_pos"], O.routing_weights(logits, ref_ids))
+        else:
+            ref_out = O.moe_layer(layer.x_np, layer.wg_np, w1, w3, w2, s.K)["out"]
+        G.check_output(g["out"][ok], ref_out[ok], "layer output vs oracle end to end")
 
 
 def test_tiny_layer_end_to_end():
@@ -79,7 +86,7 @@ def test_qwen_controlled_union(qwen_layer, U):
     _full_check(qwen_layer, g, False, routing=(ids.astype(np.int64), w))
 
 
-@pytest.mark.parametrize("T", [1, 8, 16, 17, 128, 256])
+@pytest.mark.parametrize("T", [1, 8, 16, 17, 32, 128, 256])
 def test_qwen_batch_sweep(T):
     G.say(f"case: qwen layer, controlled union U=32, batch T={T}")
     layer = G.Layer(QWEN, T)
@@ -359,21 +366,91 @@ def test_deterministic(qwen_layer):
         assert np.array_equal(a[key], b[key]), key
 
 
-def test_gpt_oss_layer_sampled():
-    # Full gpt-oss shape (6.4 GB of bf16 experts); the oracle checks a sample of tokens.
-    G.say("case: gpt-oss-shaped layer E=128 top-4 H=I=2880 T=256, gate-routed, sampled tokens")
-    layer = G.Layer(GPTOSS, 256, experts_on_host=False)
-    g = layer.run()
+@pytest.fixture(scope="module")
+def gpt_oss_layer():
+    # Full gpt-oss shape: 6.4 GB of bf16 experts on the device and a host copy
+    # of their bit patterns for the oracle.
+    G.say("building the gpt-oss-shaped layer (E=128 top-4 H=I=2880, bf16 experts), T=256")
+    return G.Layer(GPTOSS, 256)
+
+
+def test_gpt_oss_layer_gate_routed(gpt_oss_layer):
+    # Every output row and every slot row against the oracle.
+    G.say("case: gpt-oss-shaped layer T=256, gate-routed, all 256 tokens and 1024 slots")
+    g = gpt_oss_layer.run()
     G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
-    near = G.check_gate(g, layer.x_np, layer.wg_np, GPTOSS.K)
-    ids = g["ids"].astype(np.int64)
-    G.compare_buckets(g, ids, GPTOSS.E)
-    sample = [t for t in (0, 1, 77, 128, 200, 255) if not near[t]]
-    experts = sorted(set(ids[sample].ravel().tolist()))
-    w1, w3, w2 = layer.host_weights(experts)
-    sub = O.moe_layer_routed(layer.x_np[sample], ids[sample], g["weights"][sample].astype(np.float64),
-                             w1, w3, w2, GPTOSS.E)
-    G.check_output(g["out"][sample], sub["out"], "sampled tokens")
+    assert g["y_slots"].shape[0] == 256 * GPTOSS.K
+    _full_check(gpt_oss_layer, g, True)
+
+
+@pytest.mark.parametrize("U", [32, 128])
+def test_gpt_oss_controlled_union(gpt_oss_layer, U):
+    G.say(f"case: gpt-oss-shaped layer T=256, controlled union U={U}, all tokens and slots")
+    ids, w, _ = synth.controlled_routing(256, GPTOSS.E, GPTOSS.K, U, seed=U)
+    g = gpt_oss_layer.run(routing=(ids, w))
+    G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
+    assert g["union_size"] == len(set(ids.ravel().tolist()))
+    _full_check(gpt_oss_layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+@pytest.mark.parametrize("T,heavy", [(24, [(10, 24), (20, 17)]),
+                                     (32, [(3, 17), (40, 24), (77, 32)])])
+def test_two_tile_pass(T, heavy):
+    # 16 < T <= 32 takes the two-tile kernel; buckets of 17, 24 and 32 tokens
+    # run its two-tile pass (the other buckets, of a few tokens, its one-tile pass).
+    G.say(f"case: qwen layer T={T}, buckets of {[n for _, n in heavy]} tokens (two-tile pass)")
+    ids, w = G.fixed_bucket_routing(T, QWEN.E, QWEN.K, heavy, seed=T)
+    layer = G.Layer(QWEN, T, seed=50 + T)
+    g = layer.run(routing=(ids, w))
+    assert [int(g["counts"][e]) for e, _ in heavy] == [n for _, n in heavy]
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+def test_forced_near_tie():
+    # Gate rows 5 and 9 differ only by 2^-20 at hidden position 200, so
+    # logit 9 - logit 5 = 2^-20 x[200]: tokens where those two compete for the
+    # second of K = 2 places are near-ties by construction.  Every row is
+    # otherwise one-hot, so each fp32 logit is exact or takes one rounding.
+    #   t % 4 == 0, 1: x[200] = +-3, a gap of 2.9e-6 that fp32 resolves: the
+    #                  GPU picks what the oracle picks;
+    #   t % 4 == 2:    x[200] = +-0.1, a gap of 9.5e-8, below half an ulp of 2:
+    #                  the GPU's logits tie exactly and the lower id 5 wins,
+    #                  while for x[200] > 0 the oracle picks 9;
+    #   t % 4 == 3:    experts 2 and 7 lead by far: no near-tie.
+    T, E, H = 32, TINY.E, TINY.H
+    G.say("case: tiny shape T=32, gate rows 5 and 9 a 2^-20 step apart (forced near-ties)")
+    layer = G.Layer(TINY, T, seed=15)
+    rng = np.random.default_rng(15)
+    wg = np.zeros((E, H), np.float32)
+    wg[np.arange(E), np.arange(E)] = 1.0
+    wg[9, 9] = 0.0
+    wg[9, 5] = 1.0
+    wg[9, 200] = 2.0 ** -20
+    x = rng.uniform(-0.5, 0.5, (T, H)).astype(np.float32)
+    for t in range(T):
+        kind = t % 4
+        x[t, 2] = 4.0
+        if kind < 3:
+            x[t, 5] = 2.0
+            mag = 3.0 if kind < 2 else 0.1
+            sign = (1.0 if kind == 0 else -1.0) if kind < 2 else (1.0 if (t // 4) % 2 == 0 else -1.0)
+            x[t, 200] = sign * mag
+        else:
+            x[t, 7] = 2.0
+            x[t, 5] = -3.0
+    layer.x_np, layer.wg_np = x, wg
+    layer.x = torch.from_numpy(x).cuda()
+    layer.wg = torch.from_numpy(wg).cuda()
+    g = layer.run()
+    logits = O.gate_logits(x, wg)
+    near = O.selection_gaps(logits, TINY.K) < G.NEAR_TIE
+    assert near.sum() == 24 and not near[3::4].any()
+    ref = O.select_experts(logits, TINY.K)
+    differ = [t for t in range(T) if set(ref[t].tolist()) != set(g["ids"][t].tolist())]
+    G.say(f"  tokens where the GPU's valid pick differs from the oracle's: {differ}")
+    assert differ == [t for t in range(2, T, 8)]  # x[200] = +0.1: the oracle picks 9, the GPU 5
+    assert all(sorted(g["ids"][t].tolist()) == [2, 5] for t in differ)
+    _full_check(layer, g, True)
 
 
 def test_graph_replay_matches_eager():

@@ -122,3 +122,37 @@ def test_invalid_arguments_rejected():
     assert lib.eldr_balanced_kmeans(None, 4, 2, 8, None, 10, None, None, None) == B.MOE_ERR_INVALID
     with pytest.raises(B.MoeError):
         B.eldr_signature(np.zeros((2, 4), np.int32), np.ones((2, 4), np.float32), [0, 2])  # layer 2 >= L
+
+
+def test_route_rejects_bad_band_and_non_finite_signatures():
+    # A negative or NaN band width, or a NaN in the signature or the centroids,
+    # leaves no worker in the band: an error, never worker -1 reported as OK and
+    # never a load written outside the caller's buffer.
+    rng = np.random.default_rng(3)
+    C = rng.standard_normal((4, 16)).astype(np.float32)
+    s = rng.standard_normal(16).astype(np.float32)
+    loads = np.zeros(4, np.int32)
+    assert 0 <= B.eldr_route(s, C, loads, 0.1) < 4
+    for tau in (-0.1, float("nan"), float("inf")):
+        with pytest.raises(B.MoeError):
+            B.eldr_route(s, C, loads, tau)
+        with pytest.raises(B.MoeError):
+            B.eldr_route_batch(np.stack([s, s]), C, loads, tau)
+    bad = s.copy()
+    bad[3] = np.nan
+    with pytest.raises(B.MoeError):
+        B.eldr_route(bad, C, loads, 0.1)
+    C_bad = C.copy()
+    C_bad[:, 0] = np.nan
+    with pytest.raises(B.MoeError):
+        B.eldr_route(s, C_bad, loads, 0.1)
+    # in a batch, routing stops at the first request with no worker: the one
+    # before it keeps its worker and its load, nothing after it adds load
+    S = np.stack([s, bad, s])
+    ld = np.zeros(4, np.int32)
+    w = np.full(3, 7, np.int32)
+    st = B.load().eldr_route_batch(S.ctypes.data, 3, 16, C.ctypes.data, 4, ld.ctypes.data,
+                                   0.1, w.ctypes.data)
+    assert st == B.MOE_ERR_INVALID
+    assert 0 <= w[0] < 4 and w[1] == -1 and w[2] == -1
+    assert ld.sum() == 1 and ld[w[0]] == 1
