@@ -14,9 +14,11 @@ The timed layer steps are HIP graph replays, each graph holding several
 consecutive layer steps (as a captured decode step holds its layers), so host
 launch cost is not in the GPU timeline.  Printed: one JSON line with the layer's achieved algorithmic GB/s
 (the metric), the roofline of the dominant kernel (the FFN up projection,
-timed with HIP events on the stream it runs on), and the CPU oracle's rate on
-the host cores.  ``--sweep PATH`` also writes the controlled-union and batch
-sweeps (one JSON object per point) to PATH.
+timed with HIP events on the stream it runs on), the CPU oracle's rate on
+the host cores, and the controlled-union and batch sweeps of the paper's
+motivating measurement with a least-squares fit of latency against the union
+(``--no-sweep`` leaves them out; ``--sweep PATH`` also writes them to PATH as
+JSON lines; ``--point T:U`` times single controlled points only).
 """
 from __future__ import annotations
 
@@ -78,8 +80,8 @@ def layer_bytes(shape: synth.LayerShape, T: int, U: int, gate: bool) -> int:
 
 
 def up_bytes(shape: synth.LayerShape, T: int, U: int) -> int:
-    """Algorithmic bytes of one FFN up-projection launch: W1 and W3 of the union, and x."""
-    return U * 2 * shape.H * shape.I * 2 + 4 * T * shape.H
+    """Algorithmic bytes of one routed up launch: W1 and W3 of the union, x and the routing ids."""
+    return U * 2 * shape.H * shape.I * 2 + 4 * T * shape.H + 4 * T * shape.K
 
 
 def mx_matrix_bytes(shape: synth.LayerShape) -> int:
@@ -98,7 +100,9 @@ def mx_up_bytes(shape: synth.LayerShape, T: int, U: int) -> int:
 
 
 class Bench:
-    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0):
+    def __init__(self, shape: synth.LayerShape, T: int, seed: int = 0, share: "Bench | None" = None):
+        """One layer at batch T.  With ``share``, the packed expert weights (and
+        their rotation copies) of another bench of the same shape are reused."""
         self.shape = shape
         self.T = T
         self.d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
@@ -106,9 +110,13 @@ class Bench:
         self.wg_np = synth.gate_weights(shape, seed)
         self.x = torch.from_numpy(self.x_np).cuda()
         self.wg = torch.from_numpy(self.wg_np).cuda()
-        raw = synth.expert_weights(shape, seed, device="cuda")
-        self.raw_weights = raw  # row-major, for the CPU baseline
-        self.weights = [B.pack_expert_weights(*raw)]  # packed once, before any timing
+        if share is not None:
+            self.raw_weights = share.raw_weights
+            self.weights = share.weights  # the same list: copies made by either are shared
+        else:
+            raw = synth.expert_weights(shape, seed, device="cuda")
+            self.raw_weights = raw  # row-major, for the CPU baseline
+            self.weights = [B.pack_expert_weights(*raw)]  # packed once, before any timing
         self.buf = B.LayerBuffers.allocate(self.d)
         self.stream = torch.cuda.current_stream()
 
@@ -125,11 +133,11 @@ class Bench:
         ids, w = (b.topk_ids, b.topk_w) if routing is None else routing
         if routing is None:
             B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
-        B.moe_bucket(ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
-                     b.union_size)
         if ev is not None:
             ev[0].record(self.stream)
-        B.moe_expert_ffn_up(self.x, w13, b.offsets, b.perm_token, b.union_ids, b.union_size, d, b.ws)
+        # buckets and the up projection (one launch up to 64 tokens, else two)
+        B.moe_expert_ffn_up_routed(self.x, w13, ids, d, b.counts, b.offsets, b.perm_token,
+                                   b.pair_pos, b.union_ids, b.union_size, b.ws)
         if ev is not None:
             ev[1].record(self.stream)
         B.moe_expert_ffn_down(b.ws, w2, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
@@ -242,12 +250,10 @@ class MxBench(Bench):
         ids, w = (b.topk_ids, b.topk_w) if routing is None else routing
         if routing is None:
             B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
-        B.moe_bucket(ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
-                     b.union_size)
         if ev is not None:
             ev[0].record(self.stream)
-        B.moe_expert_ffn_mxfp4_up(self.x, up, b.offsets, b.perm_token, b.union_ids, b.union_size,
-                                  d, b.ws)
+        B.moe_expert_ffn_mxfp4_up_routed(self.x, up, ids, d, b.counts, b.offsets, b.perm_token,
+                                         b.pair_pos, b.union_ids, b.union_size, b.ws)
         if ev is not None:
             ev[1].record(self.stream)
         B.moe_expert_ffn_mxfp4_down(b.ws, down, b.offsets, b.perm_token, b.union_ids, b.union_size,
@@ -426,50 +432,75 @@ def host_threads() -> int:
     return max(1, min(16, n))
 
 
-def sweep(path: str, steps: int, warmup: int) -> None:
-    """Controlled-union sweep (T=64, U in 16..128) and batch sweep (U=32, T in 8..256)."""
+UNION_SWEEP = (16, 32, 64, 96, 128)       # controlled unions at T = 64
+BATCH_SWEEP = (8, 16, 32, 64, 128, 256)   # decode batches at U = 32
+
+
+def controlled_point(bench: "Bench", U: int, steps: int, warmup: int) -> dict:
+    """Time the layer at batch bench.T with a controlled union of U experts
+    (gate bypassed); bytes and rates count the realised union."""
+    shape, T = bench.shape, bench.T
+    ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0)
+    routing = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
+    bench.step(0, routing)
+    Ur = bench.union()
+    bench.rotate(Ur * shape.expert_bytes)
+    r = bench.time(steps, warmup, routing)
+    lb = layer_bytes(shape, T, Ur, False)
+    rec = {"T": T, "U_nominal": U, "U": Ur, "layer_us": round(r["layer_ms"] * 1e3, 2),
+           "layer_GBps": round(lb / r["layer_ms"] / 1e6, 1),
+           "frac_of_peak": round(lb / r["layer_ms"] / 1e6 / HBM_PEAK_GBS, 4),
+           "up_us": round(r["up_ms"] * 1e3, 2), "down_us": round(r["down_ms"] * 1e3, 2),
+           "up_frac_of_peak": round(up_bytes(shape, T, Ur) / r["up_ms"] / 1e6 / HBM_PEAK_GBS, 4)}
+    log(f"T={T} U={Ur}: layer {rec['layer_us']:.1f} us ({rec['layer_GBps']:.0f} GB/s, "
+        f"{100 * rec['frac_of_peak']:.1f}% of peak), up {rec['up_us']:.1f} us, down {rec['down_us']:.1f} us")
+    return rec
+
+
+def sweep(steps: int, warmup: int, path: str = "") -> dict:
+    """The paper's motivating measurement on this layer (Motivation, "Active
+    Expert Count Drives MoE Decode Latency"): latency against the union at a
+    fixed batch (T = 64, U = 16 .. 128), and against the batch at a fixed union
+    (U = 32, T = 8 .. 256), with a least-squares fit t = a + b U over the first.
+    All points share one weight set (and its rotation copies)."""
     shape = synth.SHAPES["qwen3_30b_a3b"]
-    points = [(64, U) for U in (16, 32, 64, 96, 128)] + [(T, 32) for T in (8, 16, 32, 64, 128, 256)]
-    with open(path, "w") as f:
-        for T, U in points:
-            bench = Bench(shape, T)
-            ids, w, _ = synth.controlled_routing(T, shape.E, shape.K, U, seed=0)
-            routing = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
-            bench.step(0, routing)
-            Ur = bench.union()
-            bench.rotate(Ur * shape.expert_bytes)
-            r = bench.time(steps, warmup, routing)
-            rec = {"T": T, "U_nominal": U, "U": Ur, "layer_us": r["layer_ms"] * 1e3,
-                   "layer_GBps": layer_bytes(shape, T, Ur, False) / r["layer_ms"] / 1e6,
-                   "up_us": r["up_ms"] * 1e3, "down_us": r["down_ms"] * 1e3,
-                   "ffn_GBps": Ur * shape.expert_bytes / (r["up_ms"] + r["down_ms"]) / 1e6}
-            rec["frac_of_peak"] = rec["layer_GBps"] / HBM_PEAK_GBS
-            f.write(json.dumps(rec) + "\n")
-            f.flush()
-            log(f"sweep T={T} U={Ur}: {rec['layer_us']:.1f} us, {rec['layer_GBps']:.0f} GB/s")
-            del bench
-            torch.cuda.empty_cache()
-    # least-squares t = a + b U over the union sweep
-    recs = [json.loads(l) for l in open(path)][:5]
-    Us = np.array([r["U"] for r in recs], float)
-    ts = np.array([r["layer_us"] for r in recs], float)
+    base = Bench(shape, 64)
+    union_pts = [controlled_point(base, U, steps, warmup) for U in UNION_SWEEP]
+    batch_pts = []
+    for T in BATCH_SWEEP:
+        if T == 64:  # the union sweep's U = 32 point is this batch point
+            batch_pts.append(next(r for r in union_pts if r["U_nominal"] == 32))
+            continue
+        bench = Bench(shape, T, share=base)
+        batch_pts.append(controlled_point(bench, 32, steps, warmup))
+        del bench
+    del base
+    torch.cuda.empty_cache()
+    Us = np.array([r["U"] for r in union_pts], float)
+    ts = np.array([r["layer_us"] for r in union_pts], float)
     b, a = np.polyfit(Us, ts, 1)
     r2 = 1 - ((ts - (a + b * Us)) ** 2).sum() / ((ts - ts.mean()) ** 2).sum()
-    with open(path, "a") as f:
-        f.write(json.dumps({"fit": "layer_us = a + b * U", "a_us": a, "b_us_per_expert": b,
-                            "r2": r2, "per_expert_GBps": shape.expert_bytes / b / 1e3}) + "\n")
-    log(f"fit: t = {a:.2f} + {b:.3f} U us (R^2 {r2:.4f})")
-    # The paper's motivating figure, for context only: on one MI300X with vLLM's
-    # MoE kernels the layer's latency rises 4.7x as the active experts go from
-    # 16 to 128 at decode batch 64 (Motivation, "Active Expert Count Drives MoE
-    # Decode Latency").  The same ratio here, largest realised union over U=16:
-    ratio = ts[-1] / ts[0]
-    with open(path, "a") as f:
-        f.write(json.dumps({"latency_ratio_largest_union_over_U16": ratio, "union_from": int(Us[0]),
-                            "union_to": int(Us[-1]), "paper_ratio_16_to_128": 4.7,
-                            "paper_hardware": "1x MI300X, vLLM MoE kernels (context, not a target)"})
-                + "\n")
-    log(f"latency ratio U={int(Us[-1])} / U={int(Us[0])}: {ratio:.2f} (paper, MI300X: 4.7 for 16 -> 128)")
+    t64 = next(r["layer_us"] for r in batch_pts if r["T"] == 64)
+    out = {"union_sweep_T64": union_pts, "batch_sweep_U32": batch_pts,
+           "fit": {"model": "layer_us = a + b * U (union sweep)", "a_us": round(a, 2),
+                   "b_us_per_expert": round(b, 4), "r2": round(r2, 5),
+                   "per_expert_GBps": round(shape.expert_bytes / b / 1e3, 1),
+                   "intercept_in_experts": round(a / b, 1)},
+           # the paper's motivating figure, context only: on one MI300X with
+           # vLLM's MoE kernels the layer's latency rises 4.7x as the active
+           # experts go from 16 to 128 at decode batch 64
+           "latency_ratio_largest_union_over_U16": round(ts[-1] / ts[0], 3),
+           "paper_ratio_16_to_128": 4.7,
+           "batch_flatness_T256_over_T64": round(
+               next(r["layer_us"] for r in batch_pts if r["T"] == 256) / t64, 3)}
+    log(f"fit: t = {a:.2f} + {b:.3f} U us (R^2 {r2:.4f}); ratio U={int(Us[-1])}/U=16 "
+        f"{out['latency_ratio_largest_union_over_U16']:.2f} (paper, MI300X: 4.7)")
+    if path:
+        with open(path, "w") as f:
+            for rec in union_pts + batch_pts:
+                f.write(json.dumps(rec) + "\n")
+            f.write(json.dumps({k: v for k, v in out.items() if not k.endswith(("T64", "U32"))}) + "\n")
+    return out
 
 
 class MultiLayer:
@@ -830,7 +861,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="host time budget of the CPU-oracle baseline (0 to skip)")
-    ap.add_argument("--sweep", default="", help="also write the union and batch sweeps to this file")
+    ap.add_argument("--sweep", default="",
+                    help="also write the union and batch sweeps (which the bench line carries) to this file")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="leave the union and batch sweeps out of the bench line")
+    ap.add_argument("--point", action="append", default=[],
+                    help="T:U -- time only this controlled-union point (repeatable; no bench line)")
     ap.add_argument("--signature", default="",
                     help="also time the expert-signature cache calls, appending JSON lines to this file")
     ap.add_argument("--signature-only", action="store_true",
@@ -841,6 +877,10 @@ def main() -> int:
     ap.add_argument("--multilayer", default="",
                     help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
                          "appending JSON lines to this file")
+    ap.add_argument("--multilayer-only", action="store_true",
+                    help="run only the --multilayer measurement (no layer bench line)")
+    ap.add_argument("--multilayer-parts", default="domain,gpt_oss",
+                    help="which --multilayer workloads to run: domain and/or gpt_oss")
     ap.add_argument("--mxfp4", default="",
                     help="also run the gpt-oss-shaped layer with MXFP4 experts beside bf16 experts "
                          "and a 36-layer MXFP4 step, appending JSON lines to this file")
@@ -865,10 +905,27 @@ def main() -> int:
     if args.mxfp4_only:
         mxfp4_workload(args.mxfp4 or "mxfp4.jsonl", args.steps, args.warmup, **mx_args)
         return 0
+    if args.point:
+        shape = synth.SHAPES["qwen3_30b_a3b"]
+        base = None
+        for spec in args.point:
+            T, U = (int(v) for v in spec.split(":"))
+            bench = Bench(shape, T, share=base)
+            base = base or bench
+            print(json.dumps({"workload": "qwen3_30b_a3b moe layer, controlled union",
+                              **controlled_point(bench, U, args.steps, args.warmup)}), flush=True)
+        return 0
     if args.signature_only:
         signature_workload(args.signature or "signature.jsonl")
         if args.routing:
             routing_workload(args.routing)
+        return 0
+    if args.multilayer_only:
+        parts = args.multilayer_parts.split(",")
+        if "domain" in parts:
+            domain_workload(args.multilayer or "multilayer.jsonl", 10, 2)
+        if "gpt_oss" in parts:
+            gpt_oss_workload(args.multilayer or "multilayer.jsonl", 5, 1)
         return 0
     shape = synth.SHAPES["qwen3_30b_a3b"]
     T = 64
@@ -903,7 +960,7 @@ def main() -> int:
         "layer_frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "ffn_up_us": round(r["up_ms"] * 1e3, 2),
         "ffn_down_us": round(r["down_ms"] * 1e3, 2),
-        "roofline": {"bound": "hbm", "kernel": "ffn_kernel<up> (moe_expert_ffn_up)",
+        "roofline": {"bound": "hbm", "kernel": "ffn_kernel<up, routed> (moe_expert_ffn_up_routed: buckets + up projection)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "bytes_per_launch": ub},
@@ -919,15 +976,19 @@ def main() -> int:
             out["cpu_baseline_all_threads"] = cpu_baseline(bench, U, args.cpu_seconds / 2, threads=n)
     del bench
     torch.cuda.empty_cache()
-    if args.sweep:
-        sweep(args.sweep, max(20, args.steps // 2), args.warmup)
+    if not args.no_sweep:
+        log("union and batch sweeps (controlled routing) ...")
+        out["sweep"] = sweep(max(20, args.steps // 2), args.warmup, args.sweep)
     if args.signature:
         signature_workload(args.signature)
     if args.routing:
         routing_workload(args.routing)
     if args.multilayer:
-        domain_workload(args.multilayer, 10, 2)
-        gpt_oss_workload(args.multilayer, 5, 1)
+        parts = args.multilayer_parts.split(",")
+        if "domain" in parts:
+            domain_workload(args.multilayer, 10, 2)
+        if "gpt_oss" in parts:
+            gpt_oss_workload(args.multilayer, 5, 1)
     if args.mxfp4:
         mxfp4_workload(args.mxfp4, max(20, args.steps // 2), args.warmup, **mx_args)
     print(json.dumps(out), flush=True)

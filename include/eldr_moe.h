@@ -216,6 +216,29 @@ int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offse
                         void* stream);
 
 /*
+ * moe_expert_ffn_up_routed -- moe_bucket followed by moe_expert_ffn_up, in
+ * one launch for batches of at most 64 tokens (two launches above that).
+ * The step after the gate (Motivation, "Active Expert Count Drives MoE Decode
+ * Latency": the union of the batch's picks is what the step loads) and the
+ * first half of the expert FFN, fused so that no separate bucketing launch
+ * sits between the routing and the weight stream: every workgroup of the up
+ * projection builds the buckets of the routing in its own LDS, and one of
+ * them also writes moe_bucket's outputs for moe_expert_ffn_down and
+ * moe_combine.
+ *
+ * topk_ids [T, K] int32 (input, as for moe_bucket); counts, offsets,
+ * perm_token, pair_pos, union_ids, union_size (outputs, identical to
+ * moe_bucket's, bit for bit, invalid routing included); x, w13, ws,
+ * ws_bytes as for moe_expert_ffn_up, whose workspace result it leaves.
+ * Errors as moe_bucket and moe_expert_ffn_up; nothing is launched on an
+ * error.
+ */
+int moe_expert_ffn_up_routed(const float* x, const uint16_t* w13, const int32_t* topk_ids,
+                             moe_dims d, int32_t* counts, int32_t* offsets, int32_t* perm_token,
+                             int32_t* pair_pos, int32_t* union_ids, int32_t* union_size,
+                             void* ws, size_t ws_bytes, void* stream);
+
+/*
  * MXFP4 expert weights (Evaluation, "Models": GPT-OSS-120B is served in
  * mxfp4).  The format is the OCP Microscaling (MX) v1.0 MXFP4: blocks of 32
  * values along the reduction axis share one E8M0 scale X = 2^(code - 127);
@@ -283,6 +306,13 @@ int moe_expert_ffn_mxfp4_down(const void* ws, const uint8_t* down_codes,
                               const int32_t* perm_token, const int32_t* union_ids,
                               const int32_t* union_size, moe_dims d, size_t ws_bytes,
                               float* y_perm, void* stream);
+/* moe_expert_ffn_mxfp4_up_routed -- moe_expert_ffn_up_routed with MXFP4
+ * weights (up_codes, up_scales as for moe_expert_ffn_mxfp4_up). */
+int moe_expert_ffn_mxfp4_up_routed(const float* x, const uint8_t* up_codes,
+                                   const uint8_t* up_scales, const int32_t* topk_ids, moe_dims d,
+                                   int32_t* counts, int32_t* offsets, int32_t* perm_token,
+                                   int32_t* pair_pos, int32_t* union_ids, int32_t* union_size,
+                                   void* ws, size_t ws_bytes, void* stream);
 
 /*
  * moe_combine -- weighted unpermute: out[t, :] = sum over j = 0..K-1 (in that

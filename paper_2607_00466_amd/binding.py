@@ -53,6 +53,10 @@ _SIGNATURES = {
     "moe_ffn_workspace_bytes": (ctypes.c_size_t, [MoeDims]),
     "moe_expert_ffn": (ctypes.c_int, [_vp] * 7 + [MoeDims, _vp, _vp, ctypes.c_size_t, _vp]),
     "moe_expert_ffn_up": (ctypes.c_int, [_vp] * 6 + [MoeDims, _vp, ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_up_routed": (ctypes.c_int, [_vp] * 3 + [MoeDims] + [_vp] * 7 +
+                                 [ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_mxfp4_up_routed": (ctypes.c_int, [_vp] * 4 + [MoeDims] + [_vp] * 7 +
+                                       [ctypes.c_size_t, _vp]),
     "moe_expert_ffn_down": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, MoeDims, ctypes.c_size_t,
                                            _vp, _vp]),
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
@@ -210,6 +214,28 @@ def moe_expert_ffn_up(x, w13, offsets, perm_token, union_ids, union_size, d: Moe
         _ptr(union_size), d, _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def _need_buckets(d: MoeDims, counts, offsets, perm_token, pair_pos, union_ids, union_size):
+    _need(counts, "counts", torch.int32, d.E)
+    _need(offsets, "offsets", torch.int32, d.E + 1)
+    _need(perm_token, "perm_token", torch.int32, d.T * d.K)
+    _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
+    _need(union_ids, "union_ids", torch.int32, 2 * d.E)
+    _need(union_size, "union_size", torch.int32, 1)
+
+
+def moe_expert_ffn_up_routed(x, w13, topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos,
+                             union_ids, union_size, ws, stream=None) -> None:
+    """moe_bucket then moe_expert_ffn_up, one launch for T <= 64."""
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need_buckets(d, counts, offsets, perm_token, pair_pos, union_ids, union_size)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_up_routed", load().moe_expert_ffn_up_routed(
+        _ptr(x), _ptr(w13), _ptr(topk_ids), d, _ptr(counts), _ptr(offsets), _ptr(perm_token),
+        _ptr(pair_pos), _ptr(union_ids), _ptr(union_size), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
                         stream=None) -> None:
     _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
@@ -344,6 +370,20 @@ def moe_expert_ffn_mxfp4_up(x, up, offsets, perm_token, union_ids, union_size, d
         _ptr(union_size), d, _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def moe_expert_ffn_mxfp4_up_routed(x, up, topk_ids, d: MoeDims, counts, offsets, perm_token,
+                                   pair_pos, union_ids, union_size, ws, stream=None) -> None:
+    """moe_bucket then moe_expert_ffn_mxfp4_up, one launch for T <= 64."""
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need_mx_up(up, d)
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need_buckets(d, counts, offsets, perm_token, pair_pos, union_ids, union_size)
+    ws_bytes = _need_ws(ws, d)
+    _check("moe_expert_ffn_mxfp4_up_routed", load().moe_expert_ffn_mxfp4_up_routed(
+        _ptr(x), _ptr(up[0]), _ptr(up[1]), _ptr(topk_ids), d, _ptr(counts), _ptr(offsets),
+        _ptr(perm_token), _ptr(pair_pos), _ptr(union_ids), _ptr(union_size), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
 def moe_expert_ffn_mxfp4_down(ws, down, offsets, perm_token, union_ids, union_size, d: MoeDims,
                               y_perm, stream=None) -> None:
     _need_mx_down(down, d)
@@ -404,39 +444,54 @@ class LayerBuffers:
         )
 
 
-def _gate_and_bucket(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream):
-    """Gate (unless routing is given) and buckets; returns the routing weights to combine with."""
+def _gate(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream):
+    """The gate (unless routing is given); returns the routing (ids, weights)."""
     if routing is None:
         moe_gate_topk(x, w_gate, d, buf.logits, buf.topk_ids, buf.topk_w, stream)
-        ids, w = buf.topk_ids, buf.topk_w
-    else:
-        ids, w = routing
-    moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
-               buf.union_size, stream)
-    return w
+        return buf.topk_ids, buf.topk_w
+    return routing
 
 
-def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
-    """One decode-step MoE layer: the four calls back to back on one stream.
+def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None,
+              fused: bool = True):
+    """One decode-step MoE layer on one stream: gate, buckets + up projection
+    (moe_expert_ffn_up_routed), down projection, combine.
 
     w13 and w2 are the expert weights packed by ``pack_expert_weights``.
 
     ``routing=(topk_ids, topk_w)`` (int32 [T, K] and fp32 [T, K] device
-    tensors) bypasses the gate: the bucket and the combine read them in place.
-    Returns ``buf.out``.
+    tensors) bypasses the gate: the buckets and the combine read them in place.
+    ``fused=False`` makes the buckets a separate moe_bucket call.  Returns ``buf.out``.
     """
-    w = _gate_and_bucket(x, w_gate, d, buf, routing, stream)
-    moe_expert_ffn(x, w13, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
-                   buf.y_perm, buf.ws, stream)
+    ids, w = _gate(x, w_gate, d, buf, routing, stream)
+    if fused:
+        moe_expert_ffn_up_routed(x, w13, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                                 buf.pair_pos, buf.union_ids, buf.union_size, buf.ws, stream)
+    else:
+        moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
+                   buf.union_size, stream)
+        moe_expert_ffn_up(x, w13, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
+                          buf.ws, stream)
+    moe_expert_ffn_down(buf.ws, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
+                        buf.y_perm, stream)
     moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 
 
-def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None):
+def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None,
+                    fused: bool = True):
     """moe_layer with MXFP4 experts: ``up`` and ``down`` from pack_mxfp4_expert_weights."""
-    w = _gate_and_bucket(x, w_gate, d, buf, routing, stream)
-    moe_expert_ffn_mxfp4(x, up, down, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
-                         d, buf.y_perm, buf.ws, stream)
+    ids, w = _gate(x, w_gate, d, buf, routing, stream)
+    if fused:
+        moe_expert_ffn_mxfp4_up_routed(x, up, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                                       buf.pair_pos, buf.union_ids, buf.union_size, buf.ws, stream)
+    else:
+        moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
+                   buf.union_size, stream)
+        moe_expert_ffn_mxfp4_up(x, up, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
+                                d, buf.ws, stream)
+    moe_expert_ffn_mxfp4_down(buf.ws, down, buf.offsets, buf.perm_token, buf.union_ids,
+                              buf.union_size, d, buf.y_perm, stream)
     moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 

@@ -96,14 +96,14 @@ __host__ __device__ constexpr int slot_steps() {
   return FMT == kBf16 ? 1 : 2;
 }
 
-// Token tiles of 16 per item: at most 64 tokens of an expert (a larger bucket
-// takes more token groups, served from L2).
+// Token tiles of 16 per item: at most 128 tokens of an expert for bf16 (64
+// for MXFP4); a larger bucket takes more token groups, served from L2.
 template <int FMT>
 __host__ __device__ constexpr int max_tiles() {
 #ifndef ELDR_FFN_FP4_MAX_TILES
 #define ELDR_FFN_FP4_MAX_TILES 4
 #endif
-  return FMT == kBf16 ? 4 : ELDR_FFN_FP4_MAX_TILES;
+  return FMT == kBf16 ? 8 : ELDR_FFN_FP4_MAX_TILES;
 }
 
 // Ring slots of weights in flight per wave (the prefetch depth of the ring;
@@ -115,7 +115,8 @@ __host__ __device__ constexpr int ring_depth() {
 }
 
 // k-steps per staged chunk: a whole number of ring cycles, as many as keep
-// one chunk of NT * 16 tokens within about 33 KB of LDS.
+// one chunk of NT * 16 tokens within about 34 KB of LDS -- except for 128
+// tokens, whose chunks are half a ring cycle (2 k-steps) and are run in pairs.
 #ifndef ELDR_FFN_CYCLES1
 #define ELDR_FFN_CYCLES1 2
 #endif
@@ -132,7 +133,8 @@ __host__ __device__ constexpr int chunk_steps() {
              ? (NT == 1   ? 2 * ELDR_FFN_FP4_CHUNK
                 : NT == 2 ? ELDR_FFN_FP4_CHUNK
                           : ELDR_FFN_FP4_CHUNK / 2)
-             : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
+             : NT == 8 ? ring_depth<FMT, NT>() / 2
+                       : ring_depth<FMT, NT>() * (NT == 1 ? ELDR_FFN_CYCLES1 : NT == 2 ? ELDR_FFN_CYCLES2 : 1);
 }
 
 #ifndef ELDR_FFN_MAX_CHUNK
@@ -187,6 +189,15 @@ struct FfnArgs {
   int experts;                 // E
   const u32x4* qcodes;         // MXFP4: packed FP4 codes (up: W1 and W3; down: W2)
   const uint32_t* qscales;     // MXFP4: packed E8M0 scales
+  // Routed up launches (the buckets built in the kernel from the routing):
+  const int32_t* ids;          // [T, K] each token's experts
+  int T, K;
+  int32_t* b_counts;           // moe_bucket's outputs, written by workgroup 0
+  int32_t* b_offsets;
+  int32_t* b_perm_token;
+  int32_t* b_pair_pos;
+  int32_t* b_union_ids;
+  int32_t* b_union_size;
 };
 
 // Rows per workgroup: up -> 16 rows per wave (each wave reads the same 16
@@ -272,8 +283,10 @@ __device__ __forceinline__ int wave_inclusive_sum(int x) {
   return x;
 }
 
-template <int MODE, int NT, bool MULTI, int FMT>
-__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs a) {
+template <int MODE, int NT, bool MULTI, int FMT, bool ROUTED>
+// (128-token passes: held to two waves a SIMD, the LDS limit, so registers never lower it)
+__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) __attribute__((amdgpu_waves_per_eu(NT == 8 ? 2 : 1)))
+void ffn_kernel(FfnArgs a) {
   constexpr int kFfnThreads = ffn_threads<MODE, FMT>();
   constexpr int kBuf = lds_buf_bytes<FMT, NT>();
   constexpr int kRing = ring_depth<FMT, NT>();
@@ -391,7 +404,9 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     };
     auto stage_tokens = [&]() {
       __syncthreads();  // the previous item has finished with LDS
-      if (tid < c) tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
+      // (a routed launch has listed the tokens already)
+      if (!ROUTED && tid < c)
+        tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
       __syncthreads();
     };
 
@@ -411,7 +426,12 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
       constexpr int kStride = 128 * kChunk + 16;  // bytes per staged token row: an odd multiple of 16
       // ring slots this pass keeps in flight
       constexpr int kRingP = FMT == kBf16 ? kRing : min_c(kRing, kChunk / kSlot);
-      static_assert(kChunk % (kRingP * kSlot) == 0, "a chunk is a whole number of ring cycles");
+      // A chunk is a whole number of ring cycles, or (128 token rows) half of
+      // one: then chunks run in kPhases consecutive phases, chunk c in phase
+      // c % kPhases, whose ring slots start kChunk k-steps further round.
+      constexpr int kPhases = kChunk >= kRingP * kSlot ? 1 : kRingP * kSlot / kChunk;
+      static_assert(kPhases == 1 ? kChunk % (kRingP * kSlot) == 0 : kPhases * kChunk == kRingP * kSlot,
+                    "a chunk is a whole number of ring cycles, or an exact fraction of one");
       static_assert(NTB * 16 * kStride <= kBuf, "a chunk fits its buffer");
       constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
       static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
@@ -482,8 +502,8 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
       // is issued after the MFMAs that read the slot, into the same
       // registers, and a scheduling barrier keeps it there, so each slot
       // stays in place and kRingP slots of loads are always in flight.
-      auto kstep = [&](auto I, int s, const unsigned char* bb, int ks) {
-        constexpr int i = (decltype(I)::value / kSlot) % kRingP;
+      auto kstep = [&](auto PH, auto I, int s, const unsigned char* bb, int ks) {
+        constexpr int i = ((decltype(PH)::value * kChunk + decltype(I)::value) / kSlot) % kRingP;
         constexpr int j = decltype(I)::value % kSlot;
         const unsigned char* bs = bb + (s - ks) * 128;
         u32x4 a0, a1;
@@ -514,35 +534,48 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
         __builtin_amdgcn_sched_barrier(0);
       };
 
-      // Chunk 0 is staged before the loop.  Each iteration then fetches the
-      // next chunk (always issued: the last full chunk fetches the tail chunk,
-      // or itself again), runs kChunk k-steps, unrolled, and publishes the next
+      // Chunk 0 is staged before the loop.  Each chunk then fetches the next
+      // one (always issued: the last full chunk fetches the tail chunk, or
+      // itself again), runs kChunk k-steps, unrolled, and publishes the next
       // chunk into the other buffer.  In steady state the staged groups are
       // older than the weight loads behind them, so a publish waits for them
-      // alone.  Chunk starts are multiples of the ring cycle (kRingP slots),
-      // so step ks + I sits in ring slot (I / kSlot) % kRingP.  The buffer
-      // published at the end of iteration ch was last read in iteration
-      // ch - 1, before the previous barrier.
+      // alone.  Chunk c starts at k-step c * kChunk, a multiple of the ring
+      // cycle plus kChunk * (c % kPhases), so its step I sits in ring slot
+      // (kChunk * (c % kPhases) + I) / kSlot mod kRingP, a constant of the
+      // phase.  The buffer published at the end of chunk c was last read in
+      // chunk c - 1, before the previous barrier.
       const int nfull = nk / kChunk;
       const int last_start = ((nk - 1) / kChunk) * kChunk;
-      fetch(0);
-      publish(0);
-      __syncthreads();
-      for (int ch = 0; ch < nfull; ++ch) {
+      auto chunk = [&](auto PH, const int ch) {
         const int ks = ch * kChunk;
         const int next = min(ks + kChunk, last_start);
         fetch(next);
         const unsigned char* bb = &lds[ch & 1][kgrp * 32];
-        static_for<kChunk>([&](auto I) { kstep(I, ks + decltype(I)::value, bb, ks); });
+        static_for<kChunk>([&](auto I) { kstep(PH, I, ks + decltype(I)::value, bb, ks); });
         publish((ch + 1) & 1);
         __syncthreads();
+      };
+      fetch(0);
+      publish(0);
+      __syncthreads();
+      const int nround = nfull - nfull % kPhases;
+      for (int ch = 0; ch < nround; ch += kPhases)
+        static_for<kPhases>([&](auto PH) { chunk(PH, ch + decltype(PH)::value); });
+      if constexpr (kPhases > 1) {
+        static_for<kPhases - 1>([&](auto PH) {
+          if (decltype(PH)::value < nfull - nround) chunk(PH, nround + decltype(PH)::value);
+        });
       }
       // Tail chunk (when nk is not a multiple of kChunk), already staged.
       if (nfull * kChunk < nk) {
         const int ks = nfull * kChunk;
         const unsigned char* bb = &lds[nfull & 1][kgrp * 32];
-        static_for<kChunk>([&](auto I) {
-          if (ks + decltype(I)::value < nk) kstep(I, ks + decltype(I)::value, bb, ks);
+        static_for<kPhases>([&](auto PH) {
+          if (nfull % kPhases == decltype(PH)::value) {
+            static_for<kChunk>([&](auto I) {
+              if (ks + decltype(I)::value < nk) kstep(PH, I, ks + decltype(I)::value, bb, ks);
+            });
+          }
         });
       }
 
@@ -583,14 +616,165 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     } else if constexpr (NT == 2) {
       if (nt == 1) run_pass(Int<1>{});
       else run_pass(Int<2>{});
-    } else {
+    } else if constexpr (NT == 4) {
       if (nt == 1) run_pass(Int<1>{});
       else if (nt == 2) run_pass(Int<2>{});
-      else run_pass(Int<NT>{});
+      else run_pass(Int<4>{});
+    } else {
+      static_assert(NT == 8, "token tiles per item: 1, 2, 4 or 8");
+      if (nt == 1) run_pass(Int<1>{});
+      else if (nt == 2) run_pass(Int<2>{});
+      else if (nt <= 4) run_pass(Int<4>{});
+      else run_pass(Int<8>{});
     }
   };
 
-  if constexpr (!MULTI) {
+  if constexpr (ROUTED) {
+    static_assert(!MULTI && MODE == kUp, "routed launches: up projection, batches of <= 64 tokens");
+    // The buckets of moe_bucket, built in LDS by every workgroup from the
+    // routing ids [T, K] (T <= 64, so a token bitmap is two words): counts,
+    // offsets, the union in dispatch order, and this item's expert and
+    // tokens; workgroup 0 also writes them out for the down projection and
+    // the combine.  Same results as moe_bucket, bit for bit.
+    __shared__ uint32_t r_mask[2 * MOE_MAX_E];
+    __shared__ __attribute__((aligned(16))) int r_key[MOE_MAX_E];
+    __shared__ int r_cnt[MOE_MAX_E], r_off[MOE_MAX_E], r_usc[MOE_MAX_E], r_rnk[MOE_MAX_E];
+    __shared__ int r_bad, r_pairs, r_union, r_e, r_present;
+    const int T = a.T, K = a.K, E = a.experts, P = a.T * a.K;
+    constexpr int kIdsPerThread = 64 * MOE_MAX_K / kFfnThreads;
+    int idv[kIdsPerThread];
+#pragma unroll
+    for (int j = 0; j < kIdsPerThread; ++j) {
+      const int p = tid + kFfnThreads * j;
+      idv[j] = p < P ? a.ids[p] : 0;
+    }
+    for (int i = tid; i < 2 * E; i += kFfnThreads) r_mask[i] = 0u;
+    if (tid == 0) {
+      r_bad = 0;
+      r_e = -1;
+      r_present = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kIdsPerThread; ++j) {
+      const int p = tid + kFfnThreads * j;
+      if (p < P) {
+        const int t = p / K;
+        const int e = idv[j];
+        if (e < 0 || e >= E) {
+          r_bad = 1;
+        } else {
+          const uint32_t bit = 1u << (t & 31);
+          if (atomicOr(&r_mask[2 * e + (t >> 5)], bit) & bit) r_bad = 1;  // an expert twice
+        }
+      }
+    }
+    __syncthreads();
+    // dispatch-order keys, larger first: 16-token tiles above 255 - e; 0 past E
+    static_assert(MOE_MAX_E <= kFfnThreads, "one expert a thread");
+    {
+      const int e = tid;
+      const int n = e < E ? __popc(r_mask[2 * e]) + __popc(r_mask[2 * e + 1]) : 0;
+      if (e < E) r_cnt[e] = n;
+      if (e < MOE_MAX_E) r_key[e] = e < E ? (((n + 15) / 16) << 8) | (MOE_MAX_E - 1 - e) : 0;
+      const unsigned long long present = __ballot(n > 0);
+      if (lane == 0) atomicAdd(&r_present, __popcll(present));
+    }
+    __syncthreads();
+    // Workgroups past the union leave here (the grid is sized from E); the
+    // first stays, to write the buckets out.
+    if ((slot / a.tiles) * kNumXcd + xcd >= r_present && blockIdx.x != 0) return;
+    if (wave == 0) {
+      // exclusive scans of the counts and of (count > 0), 4 experts a lane
+      int cv[4], sc = 0, sf = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * lane + i;
+        cv[i] = e < E ? r_cnt[e] : 0;
+        sc += cv[i];
+        sf += cv[i] > 0;
+      }
+      const int ic = wave_inclusive_sum(sc);
+      const int jf = wave_inclusive_sum(sf);
+      int bc = ic - sc, bf = jf - sf;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * lane + i;
+        if (e < E) {
+          r_off[e] = bc;
+          r_usc[e] = bf;
+        }
+        bc += cv[i];
+        bf += cv[i] > 0;
+      }
+      if (lane == kWave - 1) {
+        r_pairs = ic;
+        r_union = jf;
+      }
+    } else {
+      // dispatch position: the number of larger keys
+      for (int e = tid - kWave; e < E; e += kFfnThreads - kWave) {
+        const int key = r_key[e];
+        const int4* k4 = reinterpret_cast<const int4*>(r_key);
+        int above = 0;
+        for (int i = 0; i < MOE_MAX_E / 4; ++i) {
+          const int4 k = k4[i];
+          above += (k.x > key) + (k.y > key) + (k.z > key) + (k.w > key);
+        }
+        r_rnk[e] = above;
+      }
+    }
+    __syncthreads();
+    const bool ok = r_bad == 0 && r_pairs == P;
+    const int U = r_union;
+    const int u = (slot / a.tiles) * kNumXcd + xcd;  // this workgroup's union position
+    for (int e = tid; e < E; e += kFfnThreads)
+      if (u < U && r_rnk[e] == u) r_e = e;  // a present expert: absent ones rank from U on
+    if (blockIdx.x == 0) {
+      if (ok) {
+#pragma unroll
+        for (int j = 0; j < kIdsPerThread; ++j) {
+          const int p = tid + kFfnThreads * j;
+          if (p < P) {
+            const int t = p / K;
+            const int e = idv[j];
+            const int w = t >> 5;
+            const int below = (w ? __popc(r_mask[2 * e]) : 0) +
+                              __popc(r_mask[2 * e + w] & ((1u << (t & 31)) - 1u));
+            const int sl = r_off[e] + below;
+            a.b_perm_token[sl] = t;
+            a.b_pair_pos[p] = sl;
+          }
+        }
+      }
+      for (int e = tid; e < E; e += kFfnThreads) {
+        a.b_counts[e] = r_cnt[e];
+        a.b_offsets[e] = r_off[e];
+        if (r_cnt[e] > 0) {
+          a.b_union_ids[r_usc[e]] = e;
+          a.b_union_ids[E + r_rnk[e]] = e;
+        }
+        if (e >= U) {
+          a.b_union_ids[e] = -1;
+          a.b_union_ids[E + e] = -1;
+        }
+      }
+      if (tid == 0) {
+        a.b_offsets[E] = r_pairs;
+        *a.b_union_size = ok ? U : -1;
+      }
+    }
+    __syncthreads();
+    const int e = r_e;
+    if (!ok || e < 0) return;  // invalid routing, or no expert at this position
+    const int c = r_cnt[e];
+    if (tid < T) {
+      // the expert's tokens in ascending order: the rank of token tid's bit
+      const uint64_t m = (uint64_t)r_mask[2 * e] | ((uint64_t)r_mask[2 * e + 1] << 32);
+      if ((m >> tid) & 1u) tok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
+    }
+    run_item(Int<0>{}, e, slot % a.tiles, r_off[e], 0, c);
+  } else if constexpr (!MULTI) {
     // At most kGroupTokens tokens per expert: slot = (expert / 8) * tiles + band.
     const int u = (slot / a.tiles) * kNumXcd + xcd;
     const int U = *a.union_size;
@@ -646,39 +830,50 @@ __global__ __launch_bounds__((ffn_threads<MODE, FMT>())) void ffn_kernel(FfnArgs
     }
     const int incl = wave_inclusive_sum(lane_n);
     const int total = __builtin_amdgcn_readlane(incl, kWave - 1);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) first_j[j] += incl - lane_n;
+    if (slot >= total) return;
+    // The table moves to LDS for the item loop: held in registers it would
+    // stay live across every item and crowd the 128-token passes.
+    __shared__ int4 lk_first[kWave], lk_n[kWave], lk_c[kWave], lk_e[kWave], lk_sb[kWave];
+    if (wave == 0) {
+      const int f0 = incl - lane_n;
+      lk_first[lane] = make_int4(first_j[0] + f0, first_j[1] + f0, first_j[2] + f0, first_j[3] + f0);
+      lk_n[lane] = make_int4(n_j[0], n_j[1], n_j[2], n_j[3]);
+      lk_c[lane] = make_int4(c_j[0], c_j[1], c_j[2], c_j[3]);
+      lk_e[lane] = make_int4(e_j[0], e_j[1], e_j[2], e_j[3]);
+      lk_sb[lane] = make_int4(sb_j[0], sb_j[1], sb_j[2], sb_j[3]);
+    }
+    __syncthreads();
     for (int item = slot; item < total; item += slots) {
       // the union position whose items cover this one
+      const int4 f4 = lk_first[lane];
+      const int4 n4 = lk_n[lane];
+      const int fj[4] = {f4.x, f4.y, f4.z, f4.w};
+      const int nj[4] = {n4.x, n4.y, n4.z, n4.w};
       int js = -1, ls = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const unsigned long long hit =
-            __ballot(n_j[j] > 0 && first_j[j] <= item && item < first_j[j] + n_j[j]);
+        const unsigned long long hit = __ballot(nj[j] > 0 && fj[j] <= item && item < fj[j] + nj[j]);
         if (hit != 0) {
           js = j;
           ls = __ffsll(hit) - 1;
         }
       }
       if (js < 0) break;  // not reached: the ranges cover [0, total)
-      auto pick = [&](const int (&v)[4]) {
-        int r = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (j == js) r = __builtin_amdgcn_readlane(v[j], ls);
-        return r;
-      };
-      const int cu = pick(c_j);
+      js = __builtin_amdgcn_readfirstlane(js);
+      ls = __builtin_amdgcn_readfirstlane(ls);
+      // union position 4 * ls + js: its entries, read at a uniform address
+      auto pick = [&](const int4* v) { return reinterpret_cast<const int*>(v)[4 * ls + js]; };
+      const int cu = pick(lk_c);
       const int g = (cu + kGroupTokens - 1) / kGroupTokens;
-      const int r = item - pick(first_j);
+      const int r = item - pick(lk_first);
       const int band = r / g;
       const int group = r - band * g;
       const int tile = ((xcd - a.tiles * (4 * ls + js)) & (kNumXcd - 1)) + kNumXcd * band;
       const int p0 = group * kGroupTokens;
       const int c = min(kGroupTokens, cu - p0);
       if (c > 0) {
-        const int ie = pick(e_j);
-        const int isb = pick(sb_j);
+        const int ie = pick(lk_e);
+        const int isb = pick(lk_sb);
         if (g > 1)
           run_item(Int<1>{}, ie, tile, isb, p0, c);
         else
@@ -696,7 +891,7 @@ static int ffn_nt(int T) {
 #ifdef ELDR_FFN_FORCE_NT
   nt_T = 16 * ELDR_FFN_FORCE_NT;
 #endif
-  return nt_T <= 16 ? 1 : nt_T <= 32 ? 2 : max_tiles<FMT>();
+  return nt_T <= 16 ? 1 : nt_T <= 32 ? 2 : nt_T <= 64 ? 4 : max_tiles<FMT>();
 }
 
 // Slots per XCD: one item per (expert, band) of an XCD's share of the
@@ -706,14 +901,32 @@ static int ffn_nt(int T) {
 template <int MODE, int FMT, int NT>
 static void launch_ffn(FfnArgs a, int T, int K, int E, hipStream_t s) {
   const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
-  if (T <= NT * 16) {
-    hipLaunchKernelGGL((ffn_kernel<MODE, NT, false, FMT>), dim3(kNumXcd * a.tiles * per_xcd),
-                       dim3(ffn_threads<MODE, FMT>()), 0, s, a);
-  } else {
-    const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
-    hipLaunchKernelGGL((ffn_kernel<MODE, NT, true, FMT>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
-                       dim3(ffn_threads<MODE, FMT>()), 0, s, a);
+  // Batches of up to 64 tokens (never the 128-token kernel) deal whole
+  // experts; larger ones deal (expert, band) units, balancing skewed buckets.
+  if constexpr (NT <= 4) {
+    if (T <= NT * 16) {
+      hipLaunchKernelGGL((ffn_kernel<MODE, NT, false, FMT, false>), dim3(kNumXcd * a.tiles * per_xcd),
+                         dim3(ffn_threads<MODE, FMT>()), 0, s, a);
+      return;
+    }
   }
+  const int extra = (T * K / (NT * 16) + kNumXcd - 1) / kNumXcd;
+  hipLaunchKernelGGL((ffn_kernel<MODE, NT, true, FMT, false>), dim3(kNumXcd * a.tiles * (per_xcd + extra)),
+                     dim3(ffn_threads<MODE, FMT>()), 0, s, a);
+}
+
+// The routed up launch (batches of at most 64 tokens): the grid of the
+// whole-expert dealing, each workgroup building the buckets itself.
+template <int FMT>
+static void launch_ffn_routed(const FfnArgs& a, int T, int E, hipStream_t s) {
+  const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(kNumXcd * a.tiles * per_xcd), block(ffn_threads<kUp, FMT>());
+  if (T <= 16)
+    hipLaunchKernelGGL((ffn_kernel<kUp, 1, false, FMT, true>), grid, block, 0, s, a);
+  else if (T <= 32)
+    hipLaunchKernelGGL((ffn_kernel<kUp, 2, false, FMT, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((ffn_kernel<kUp, 4, false, FMT, true>), grid, block, 0, s, a);
 }
 
 template <int MODE, int FMT>
@@ -723,6 +936,8 @@ static void launch_ffn_nt(const FfnArgs& a, int T, int K, int E, hipStream_t s) 
     launch_ffn<MODE, FMT, 1>(a, T, K, E, s);
   else if (nt == 2)
     launch_ffn<MODE, FMT, 2>(a, T, K, E, s);
+  else if (nt == 4 || max_tiles<FMT>() == 4)
+    launch_ffn<MODE, FMT, 4>(a, T, K, E, s);
   else
     launch_ffn<MODE, FMT, max_tiles<FMT>()>(a, T, K, E, s);
 }
@@ -819,6 +1034,57 @@ extern "C" int moe_expert_ffn(const float* x, const uint16_t* w13, const uint16_
                              y_perm, stream);
 }
 
+// ---- routed up launches: moe_bucket and the up projection in one launch ------
+
+namespace {
+
+// Checks shared by the routed entry points; on success the bucket outputs
+// are valid, non-null, 4-byte aligned buffers.
+int check_routed(const moe_dims& d, const int32_t* topk_ids, const int32_t* counts,
+                 const int32_t* offsets, const int32_t* perm_token, const int32_t* pair_pos,
+                 const int32_t* union_ids, const int32_t* union_size) {
+  using namespace eldr_host;
+  if (!counts || !offsets || !perm_token || !pair_pos || !union_ids || !union_size || !topk_ids)
+    return MOE_ERR_INVALID;
+  if (!aligned4(topk_ids) || !aligned4(counts) || !aligned4(offsets) || !aligned4(perm_token) ||
+      !aligned4(pair_pos) || !aligned4(union_ids) || !aligned4(union_size))
+    return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_expert_ffn_up_routed(const float* x, const uint16_t* w13,
+                                        const int32_t* topk_ids, moe_dims d, int32_t* counts,
+                                        int32_t* offsets, int32_t* perm_token, int32_t* pair_pos,
+                                        int32_t* union_ids, int32_t* union_size, void* ws,
+                                        size_t ws_bytes, void* stream) {
+  using namespace eldr_host;
+  int st = check_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0 || d.T > 64) {
+    // nothing to multiply (moe_bucket writes the empty buckets), or too many
+    // tokens for the in-kernel buckets: the two calls
+    st = moe_bucket(topk_ids, d, counts, offsets, perm_token, pair_pos, union_ids, union_size,
+                    stream);
+    if (st != MOE_OK || d.T == 0) return st;
+    return moe_expert_ffn_up(x, w13, offsets, perm_token, union_ids, union_size, d, ws, ws_bytes,
+                             stream);
+  }
+  if (!x || !w13 || !ws) return MOE_ERR_INVALID;
+  st = check_routed(d, topk_ids, counts, offsets, perm_token, pair_pos, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(ws)) return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids + d.E,
+                   union_size, ws, d.I, d.H, 0, d.E, nullptr, nullptr,
+                   topk_ids, d.T, d.K, counts, offsets, perm_token, pair_pos, union_ids,
+                   union_size};
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kBf16>(d);
+  eldr::launch_ffn_routed<eldr::kBf16>(up, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
 // ---- MXFP4 expert weights ----------------------------------------------------
 
 namespace {
@@ -906,4 +1172,37 @@ extern "C" int moe_expert_ffn_mxfp4(const float* x, const uint8_t* up_codes,
   if (st != MOE_OK) return st;
   return moe_expert_ffn_mxfp4_down(ws, down_codes, down_scales, offsets, perm_token, union_ids,
                                    union_size, d, ws_bytes, y_perm, stream);
+}
+
+extern "C" int moe_expert_ffn_mxfp4_up_routed(const float* x, const uint8_t* up_codes,
+                                              const uint8_t* up_scales, const int32_t* topk_ids,
+                                              moe_dims d, int32_t* counts, int32_t* offsets,
+                                              int32_t* perm_token, int32_t* pair_pos,
+                                              int32_t* union_ids, int32_t* union_size, void* ws,
+                                              size_t ws_bytes, void* stream) {
+  using namespace eldr_host;
+  int st = check_mxfp4_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0 || d.T > 64) {
+    st = moe_bucket(topk_ids, d, counts, offsets, perm_token, pair_pos, union_ids, union_size,
+                    stream);
+    if (st != MOE_OK || d.T == 0) return st;
+    return moe_expert_ffn_mxfp4_up(x, up_codes, up_scales, offsets, perm_token, union_ids,
+                                   union_size, d, ws, ws_bytes, stream);
+  }
+  if (!x || !up_codes || !up_scales || !ws) return MOE_ERR_INVALID;
+  st = check_routed(d, topk_ids, counts, offsets, perm_token, pair_pos, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(up_codes) || !aligned4(up_scales) || !aligned16(ws))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, offsets, perm_token,
+                   union_ids + d.E, union_size, ws, d.I, d.H, 0, d.E,
+                   reinterpret_cast<const eldr::u32x4*>(up_codes),
+                   reinterpret_cast<const uint32_t*>(up_scales),
+                   topk_ids, d.T, d.K, counts, offsets, perm_token, pair_pos, union_ids,
+                   union_size};
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kMxfp4>(d);
+  eldr::launch_ffn_routed<eldr::kMxfp4>(up, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
 }

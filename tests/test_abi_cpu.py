@@ -203,3 +203,26 @@ def test_mxfp4_pack_arguments_rejected(lib):
     assert pd(FAKE, FAKE, 2, 32, 64, FAKE, F3, None) == B.MOE_ERR_INVALID                 # in place
     assert pd(FAKE, FAKE, 2, 32, 64, FAKE_MIS, F3, None) == B.MOE_ERR_UNSUPPORTED         # codes out
     assert pu(FAKE, FAKE, FAKE, FAKE, 0, 16, 64, None, None, None) == B.MOE_OK            # nothing to do
+
+
+def test_routed_up_validates_on_host(lib):
+    # moe_expert_ffn_up_routed / _mxfp4: the dims, null, alignment and
+    # workspace checks of moe_bucket and the up projection, before any launch.
+    fns = (lambda d, ids=FAKE, cnt=FAKE, ws_bytes=1 << 40, x=FAKE:
+           lib.moe_expert_ffn_up_routed(x, FAKE, ids, d, cnt, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                        ws_bytes, None),
+           lambda d, ids=FAKE, cnt=FAKE, ws_bytes=1 << 40, x=FAKE:
+           lib.moe_expert_ffn_mxfp4_up_routed(x, FAKE, FAKE, ids, d, cnt, FAKE, FAKE, FAKE, FAKE,
+                                              FAKE, FAKE, ws_bytes, None))
+    for f in fns:
+        assert f(B.dims(64, 2048, 128, 129, 768)) == B.MOE_ERR_INVALID         # K > E
+        assert f(B.dims(64, 2048, 257, 8, 768)) == B.MOE_ERR_UNSUPPORTED       # E above the limit
+        assert f(B.dims(*GOOD), ids=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), cnt=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), x=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), ids=ctypes.c_void_p(0x10002)) == B.MOE_ERR_UNSUPPORTED
+        assert f(B.dims(*GOOD), x=FAKE_MIS) == B.MOE_ERR_UNSUPPORTED
+        d = B.dims(*GOOD)
+        assert f(d, ws_bytes=B.moe_ffn_workspace_bytes(d) - 1) == B.MOE_ERR_WORKSPACE
+    # MXFP4 reductions must be multiples of 64
+    assert fns[1](B.dims(64, 2048 + 32, 128, 8, 768)) == B.MOE_ERR_UNSUPPORTED
