@@ -216,6 +216,28 @@ int moe_expert_ffn_down(const void* ws, const uint16_t* w2, const int32_t* offse
                         void* stream);
 
 /*
+ * moe_expert_ffn_noalloc -- moe_expert_ffn without a caller workspace, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The workspace (h of
+ * every slot, moe_ffn_workspace_bytes(d) bytes) lives in a fixed device array
+ * of moe_expert_ffn_noalloc_max_bytes() = 32 MiB inside the library, one per
+ * GPU, held until the process ends; its address is taken on the first call on
+ * each device.  The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine).  Arguments, layouts, results and errors as
+ * moe_expert_ffn; a problem whose workspace exceeds 32 MiB (T*K*I*4 bytes)
+ * returns MOE_ERR_WORKSPACE before any launch.  Every call on one GPU shares
+ * that GPU's array, which keeps the last call's contents (nothing in it needs
+ * to start at zero): calls that overlap on one GPU -- on different streams,
+ * or from different host threads without ordering -- race and must not be
+ * made.
+ */
+int moe_expert_ffn_noalloc(const float* x, const uint16_t* w13, const uint16_t* w2,
+                           const int32_t* offsets, const int32_t* perm_token,
+                           const int32_t* union_ids, const int32_t* union_size, moe_dims d,
+                           float* y_perm, void* stream);
+size_t moe_expert_ffn_noalloc_max_bytes(void);
+
+/*
  * moe_expert_ffn_up_routed -- moe_bucket followed by moe_expert_ffn_up, in
  * one launch for batches of at most 64 tokens (two launches above that).
  * The step after the gate (Motivation, "Active Expert Count Drives MoE Decode

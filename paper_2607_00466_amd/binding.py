@@ -53,6 +53,8 @@ _SIGNATURES = {
     "moe_ffn_workspace_bytes": (ctypes.c_size_t, [MoeDims]),
     "moe_expert_ffn": (ctypes.c_int, [_vp] * 7 + [MoeDims, _vp, _vp, ctypes.c_size_t, _vp]),
     "moe_expert_ffn_up": (ctypes.c_int, [_vp] * 6 + [MoeDims, _vp, ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_noalloc": (ctypes.c_int, [_vp] * 7 + [MoeDims, _vp, _vp]),
+    "moe_expert_ffn_noalloc_max_bytes": (ctypes.c_size_t, []),
     "moe_expert_ffn_up_routed": (ctypes.c_int, [_vp] * 3 + [MoeDims] + [_vp] * 7 +
                                  [ctypes.c_size_t, _vp]),
     "moe_expert_ffn_mxfp4_up_routed": (ctypes.c_int, [_vp] * 4 + [MoeDims] + [_vp] * 7 +
@@ -221,6 +223,19 @@ def _need_buckets(d: MoeDims, counts, offsets, perm_token, pair_pos, union_ids, 
     _need(pair_pos, "pair_pos", torch.int32, d.T * d.K)
     _need(union_ids, "union_ids", torch.int32, 2 * d.E)
     _need(union_size, "union_size", torch.int32, 1)
+
+
+def moe_expert_ffn_noalloc(x, w13, w2, offsets, perm_token, union_ids, union_size, d: MoeDims,
+                           y_perm, stream=None) -> None:
+    """moe_expert_ffn with the library's fixed device workspace (no caller buffer)."""
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
+    _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    _need_routing(offsets, perm_token, union_ids, union_size, d)
+    _check("moe_expert_ffn_noalloc", load().moe_expert_ffn_noalloc(
+        _ptr(x), _ptr(w13), _ptr(w2), _ptr(offsets), _ptr(perm_token), _ptr(union_ids),
+        _ptr(union_size), d, _ptr(y_perm), _stream(stream)))
 
 
 def moe_expert_ffn_up_routed(x, w13, topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos,

@@ -49,6 +49,8 @@
 //   codes are expanded to bf16 in registers by the gfx950 scaled convert
 //   right before the same MFMAs -- the products are those of the bf16 path
 //   on the dequantized weights, for about a quarter of the bytes.
+#include <mutex>
+
 #include "common.hpp"
 
 namespace eldr {
@@ -1032,6 +1034,57 @@ extern "C" int moe_expert_ffn(const float* x, const uint16_t* w13, const uint16_
   if (st != MOE_OK) return st;
   return moe_expert_ffn_down(h, w2, offsets, perm_token, union_ids, union_size, d, ws_bytes,
                              y_perm, stream);
+}
+
+// ---- the allocation-free expert FFN ---------------------------------------------
+
+// The workspace of moe_expert_ffn_noalloc: h of every slot, in a file-scope
+// device array of fixed size that each GPU the library runs on holds until the
+// process ends.  Host code never passes `scratch` itself (in host code it is
+// a stand-in, not a device address): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kNoallocScratchBytes = size_t(32) << 20;  // 32 MiB
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device.
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MOE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MOE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" size_t moe_expert_ffn_noalloc_max_bytes(void) { return kNoallocScratchBytes; }
+
+extern "C" int moe_expert_ffn_noalloc(const float* x, const uint16_t* w13, const uint16_t* w2,
+                                      const int32_t* offsets, const int32_t* perm_token,
+                                      const int32_t* union_ids, const int32_t* union_size,
+                                      moe_dims d, float* y_perm, void* stream) {
+  using namespace eldr_host;
+  int st = check_dims(d);
+  if (st != MOE_OK) return st;
+  if (d.T == 0) return MOE_OK;
+  if (moe_ffn_workspace_bytes(d) > kNoallocScratchBytes) return MOE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  st = scratch_on_current_device(&ws);
+  if (st != MOE_OK) return st;
+  return moe_expert_ffn(x, w13, w2, offsets, perm_token, union_ids, union_size, d, y_perm, ws,
+                        kNoallocScratchBytes, stream);
 }
 
 // ---- routed up launches: moe_bucket and the up projection in one launch ------

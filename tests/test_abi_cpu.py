@@ -226,3 +226,16 @@ def test_routed_up_validates_on_host(lib):
         assert f(d, ws_bytes=B.moe_ffn_workspace_bytes(d) - 1) == B.MOE_ERR_WORKSPACE
     # MXFP4 reductions must be multiples of 64
     assert fns[1](B.dims(64, 2048 + 32, 128, 8, 768)) == B.MOE_ERR_UNSUPPORTED
+
+
+def test_noalloc_ffn_rejects_oversize_on_host(lib):
+    # The fixed workspace holds 32 MiB; a larger problem is refused before the
+    # library touches a device.
+    assert lib.moe_expert_ffn_noalloc_max_bytes() == 32 << 20
+    d = B.dims(4096, 2048, 128, 16, 768)  # T*K*I*4 = 201 MB
+    assert lib.moe_expert_ffn_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, d, FAKE,
+                                      None) == B.MOE_ERR_WORKSPACE
+    assert lib.moe_expert_ffn_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                      B.dims(64, 2048, 128, 129, 768), FAKE, None) == B.MOE_ERR_INVALID
+    assert lib.moe_expert_ffn_noalloc(None, None, None, None, None, None, None,
+                                      B.dims(0, 2048, 128, 8, 768), None, None) == B.MOE_OK
