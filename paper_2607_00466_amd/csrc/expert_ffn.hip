@@ -638,10 +638,11 @@ void ffn_kernel(FfnArgs a) {
     // offsets, the union in dispatch order, and this item's expert and
     // tokens; workgroup 0 also writes them out for the down projection and
     // the combine.  Same results as moe_bucket, bit for bit.
-    __shared__ uint32_t r_mask[2 * MOE_MAX_E];
-    __shared__ __attribute__((aligned(16))) int r_key[MOE_MAX_E];
-    __shared__ int r_cnt[MOE_MAX_E], r_off[MOE_MAX_E], r_usc[MOE_MAX_E], r_rnk[MOE_MAX_E];
-    __shared__ int r_bad, r_pairs, r_union, r_e, r_present;
+    __shared__ uint32_t r_mask[2 * MOE_MAX_E];       // token bitmaps: bit t of word t / 32
+    __shared__ int r_off[MOE_MAX_E];                  // bucket offsets
+    __shared__ unsigned long long r_cls[4][4];        // [wave][class - 1] ballots
+    __shared__ int r_wn[4], r_wp[4];                  // per-wave totals: pairs, experts
+    __shared__ int r_bad, r_e;
     const int T = a.T, K = a.K, E = a.experts, P = a.T * a.K;
     constexpr int kIdsPerThread = 64 * MOE_MAX_K / kFfnThreads;
     int idv[kIdsPerThread];
@@ -654,7 +655,6 @@ void ffn_kernel(FfnArgs a) {
     if (tid == 0) {
       r_bad = 0;
       r_e = -1;
-      r_present = 0;
     }
     __syncthreads();
 #pragma unroll
@@ -672,67 +672,78 @@ void ffn_kernel(FfnArgs a) {
       }
     }
     __syncthreads();
-    // dispatch-order keys, larger first: 16-token tiles above 255 - e; 0 past E
-    static_assert(MOE_MAX_E <= kFfnThreads, "one expert a thread");
-    {
-      const int e = tid;
-      const int n = e < E ? __popc(r_mask[2 * e]) + __popc(r_mask[2 * e + 1]) : 0;
-      if (e < E) r_cnt[e] = n;
-      if (e < MOE_MAX_E) r_key[e] = e < E ? (((n + 15) / 16) << 8) | (MOE_MAX_E - 1 - e) : 0;
-      const unsigned long long present = __ballot(n > 0);
-      if (lane == 0) atomicAdd(&r_present, __popcll(present));
+    // One expert a thread.  Its count n, and its class: the 16-token tiles of
+    // its bucket (1 .. 4 here, T <= 64; 0 when absent).  The dispatch order
+    // (more tiles first, equal tiles by ascending id) ranks an expert by the
+    // experts of higher classes plus those of its class with lower ids, which
+    // per-wave ballots of each class give directly.  Offsets and ascending
+    // union positions are prefix sums: within a wave by DPP, across the
+    // four waves from their totals.
+    static_assert(MOE_MAX_E <= kFfnThreads && kFfnThreads == 4 * kWave, "one expert a thread");
+    const int me = tid;
+    const int n = me < E ? __popc(r_mask[2 * me]) + __popc(r_mask[2 * me + 1]) : 0;
+    const int cls = (n + 15) / 16;
+    const int incl_n = wave_inclusive_sum(n);
+    const int incl_p = wave_inclusive_sum(n > 0 ? 1 : 0);
+#pragma unroll
+    for (int c = 1; c <= 4; ++c) {
+      const unsigned long long b = __ballot(cls == c);
+      if (lane == 0) r_cls[wave][c - 1] = b;
+    }
+    if (lane == kWave - 1) {
+      r_wn[wave] = incl_n;
+      r_wp[wave] = incl_p;
     }
     __syncthreads();
+    int U = 0, before_n = 0, before_p = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      U += r_wp[w];
+      before_n += w < wave ? r_wn[w] : 0;
+      before_p += w < wave ? r_wp[w] : 0;
+    }
+    const int pairs = r_wn[0] + r_wn[1] + r_wn[2] + r_wn[3];
+    const int u = (slot / a.tiles) * kNumXcd + xcd;  // this workgroup's union position
     // Workgroups past the union leave here (the grid is sized from E); the
     // first stays, to write the buckets out.
-    if ((slot / a.tiles) * kNumXcd + xcd >= r_present && blockIdx.x != 0) return;
-    if (wave == 0) {
-      // exclusive scans of the counts and of (count > 0), 4 experts a lane
-      int cv[4], sc = 0, sf = 0;
+    if (u >= U && blockIdx.x != 0) return;
+    const int off = before_n + incl_n - n;
+    int rank = 0;
+    if (cls > 0) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = 4 * lane + i;
-        cv[i] = e < E ? r_cnt[e] : 0;
-        sc += cv[i];
-        sf += cv[i] > 0;
-      }
-      const int ic = wave_inclusive_sum(sc);
-      const int jf = wave_inclusive_sum(sf);
-      int bc = ic - sc, bf = jf - sf;
+      for (int c = 4; c >= 1; --c) {
+        if (c > cls) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = 4 * lane + i;
-        if (e < E) {
-          r_off[e] = bc;
-          r_usc[e] = bf;
+          for (int w = 0; w < 4; ++w) rank += __popcll(r_cls[w][c - 1]);
         }
-        bc += cv[i];
-        bf += cv[i] > 0;
       }
-      if (lane == kWave - 1) {
-        r_pairs = ic;
-        r_union = jf;
-      }
-    } else {
-      // dispatch position: the number of larger keys
-      for (int e = tid - kWave; e < E; e += kFfnThreads - kWave) {
-        const int key = r_key[e];
-        const int4* k4 = reinterpret_cast<const int4*>(r_key);
-        int above = 0;
-        for (int i = 0; i < MOE_MAX_E / 4; ++i) {
-          const int4 k = k4[i];
-          above += (k.x > key) + (k.y > key) + (k.z > key) + (k.w > key);
-        }
-        r_rnk[e] = above;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const unsigned long long b = r_cls[w][cls - 1];
+        rank += w < wave ? __popcll(b) : w == wave ? __popcll(b & ((1ull << lane) - 1ull)) : 0;
       }
     }
-    __syncthreads();
-    const bool ok = r_bad == 0 && r_pairs == P;
-    const int U = r_union;
-    const int u = (slot / a.tiles) * kNumXcd + xcd;  // this workgroup's union position
-    for (int e = tid; e < E; e += kFfnThreads)
-      if (u < U && r_rnk[e] == u) r_e = e;  // a present expert: absent ones rank from U on
+    if (me < E) r_off[me] = off;
+    if (cls > 0 && rank == u) r_e = me;
+    const bool ok = r_bad == 0 && pairs == P;
     if (blockIdx.x == 0) {
+      if (me < E) {
+        a.b_counts[me] = n;
+        a.b_offsets[me] = off;
+        if (n > 0) {
+          a.b_union_ids[before_p + incl_p - 1] = me;
+          a.b_union_ids[E + rank] = me;
+        }
+        if (me >= U) {
+          a.b_union_ids[me] = -1;
+          a.b_union_ids[E + me] = -1;
+        }
+      }
+      if (tid == 0) {
+        a.b_offsets[E] = pairs;
+        *a.b_union_size = ok ? U : -1;
+      }
+      __syncthreads();  // r_off complete (uniform: the whole of workgroup 0)
       if (ok) {
 #pragma unroll
         for (int j = 0; j < kIdsPerThread; ++j) {
@@ -749,27 +760,11 @@ void ffn_kernel(FfnArgs a) {
           }
         }
       }
-      for (int e = tid; e < E; e += kFfnThreads) {
-        a.b_counts[e] = r_cnt[e];
-        a.b_offsets[e] = r_off[e];
-        if (r_cnt[e] > 0) {
-          a.b_union_ids[r_usc[e]] = e;
-          a.b_union_ids[E + r_rnk[e]] = e;
-        }
-        if (e >= U) {
-          a.b_union_ids[e] = -1;
-          a.b_union_ids[E + e] = -1;
-        }
-      }
-      if (tid == 0) {
-        a.b_offsets[E] = r_pairs;
-        *a.b_union_size = ok ? U : -1;
-      }
     }
     __syncthreads();
     const int e = r_e;
     if (!ok || e < 0) return;  // invalid routing, or no expert at this position
-    const int c = r_cnt[e];
+    const int c = __popc(r_mask[2 * e]) + __popc(r_mask[2 * e + 1]);
     if (tid < T) {
       // the expert's tokens in ascending order: the rank of token tid's bit
       const uint64_t m = (uint64_t)r_mask[2 * e] | ((uint64_t)r_mask[2 * e + 1] << 32);
