@@ -148,6 +148,7 @@ __host__ __device__ constexpr int max_chunk() {
   return FMT == kBf16 ? ELDR_FFN_MAX_CHUNK : ELDR_FFN_FP4_MAX_CHUNK;
 }
 __host__ __device__ constexpr int min_c(int a, int b) { return a < b ? a : b; }
+__host__ __device__ constexpr int pow2_floor(int v) { return v >= 2 ? 2 * pow2_floor(v / 2) : 1; }
 
 // Bytes of one LDS staging buffer (two are used, double-buffered): NT * 16
 // token rows of chunk_steps k-steps (128 bytes each) plus 16 bytes of padding.
@@ -400,9 +401,14 @@ void ffn_kernel(FfnArgs a) {
         }
       }
     };
-    auto ring_prologue = [&](auto N_) {
+    // Ring slots [FROM, TO) of the prologue.  A CU keeps only so many loads
+    // in flight, so at an item's start the loads go out in the order the
+    // first k-step needs them: ring slot 0, then the first chunk of
+    // activations, then the rest of the ring (the publish of that chunk then
+    // waits for the activations and the slot-0 weights alone).
+    auto ring_prologue = [&](auto FROM_, auto TO_) {
 #pragma unroll
-      for (int i = 0; i < decltype(N_)::value; ++i) ring_load(i, min(i, nslot - 1));
+      for (int i = decltype(FROM_)::value; i < decltype(TO_)::value; ++i) ring_load(i, min(i, nslot - 1));
     };
     auto stage_tokens = [&]() {
       __syncthreads();  // the previous item has finished with LDS
@@ -412,10 +418,10 @@ void ffn_kernel(FfnArgs a) {
       __syncthreads();
     };
 
-    // bf16 fills the whole ring before the pass shape is chosen; MXFP4's ring
+    // bf16 issues ring slot 0 before the pass shape is chosen; MXFP4's ring
     // depth depends on the pass shape, so each pass fills its own.
     if constexpr (FMT == kBf16) {
-      ring_prologue(Int<kRing>{});
+      ring_prologue(Int<0>{}, Int<1>{});
       stage_tokens();
     }
 
@@ -424,7 +430,8 @@ void ffn_kernel(FfnArgs a) {
     // same buffer and a small bucket crosses as few barriers as a large one.
     auto run_pass = [&](auto NTB_) {
       constexpr int NTB = decltype(NTB_)::value;
-      constexpr int kChunk = min_c(chunk_steps<FMT, NT>() * NT / NTB, max_chunk<FMT>());
+      // (a power of two, so that it divides the ring cycle or a multiple of it)
+      constexpr int kChunk = pow2_floor(min_c(chunk_steps<FMT, NT>() * NT / NTB, max_chunk<FMT>()));
       constexpr int kStride = 128 * kChunk + 16;  // bytes per staged token row: an odd multiple of 16
       // ring slots this pass keeps in flight
       constexpr int kRingP = FMT == kBf16 ? kRing : min_c(kRing, kChunk / kSlot);
@@ -438,7 +445,7 @@ void ffn_kernel(FfnArgs a) {
       constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
       static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
       if constexpr (FMT == kMxfp4) {
-        ring_prologue(Int<kRingP>{});
+        ring_prologue(Int<0>{}, Int<1>{});
         stage_tokens();
       }
 
@@ -516,21 +523,54 @@ void ffn_kernel(FfnArgs a) {
           a0 = expand_fp4(ring0[i][j], rsc[i] >> (8 * j));
           a1 = expand_fp4(ring0[i][2 + j], rsc[i] >> (8 * (2 + j)));
         }
-  #pragma unroll
-        for (int t = 0; t < NTB; ++t) {
-          if (t < nt) {
-            // Column n of the product depends only on column n of B, so lanes
-            // past the bucket read its last token and their columns are
-            // simply not stored.
-            const int n = min(t * 16 + arow, c - 1);
-            const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * kStride);
-            const u32x4 bh = bp[0];
-            const u32x4 bl = bp[1];
-            acc0[t] = mfma16x16x32(a0, bh, acc0[t]);
-            acc0[t] = mfma16x16x32(a0, bl, acc0[t]);
-            acc1[t] = mfma16x16x32(a1, bh, acc1[t]);
-            acc1[t] = mfma16x16x32(a1, bl, acc1[t]);
+        if constexpr (NTB == 8) {
+          // The widest pass runs tile by tile and only over the bucket's
+          // tiles: the grouped form below needs more registers than two
+          // waves a SIMD leave it.  Lanes past the bucket read its last
+          // token; their columns are not stored.
+#pragma unroll
+          for (int t = 0; t < NTB; ++t) {
+            if (t < nt) {
+              const int n = min(t * 16 + arow, c - 1);
+              const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * kStride);
+              const u32x4 bh = bp[0];
+              const u32x4 bl = bp[1];
+              acc0[t] = mfma16x16x32(a0, bh, acc0[t]);
+              acc0[t] = mfma16x16x32(a0, bl, acc0[t]);
+              acc1[t] = mfma16x16x32(a1, bh, acc1[t]);
+              acc1[t] = mfma16x16x32(a1, bl, acc1[t]);
+            }
           }
+        } else {
+          // Token tiles in groups of up to 4: the group's B operands are read
+          // from LDS first, then its high-part products, then its low-part
+          // ones (the two products into one accumulator are a group apart).
+          // Every tile of the pass is multiplied: column n of the product
+          // depends only on column n of B, so lanes past the bucket read its
+          // last token, and tiles and columns past it are simply not stored.
+          constexpr int kGrp = NTB <= 4 ? NTB : 2;
+          static_assert(NTB % kGrp == 0, "whole tile groups");
+          static_for<NTB / kGrp>([&](auto G) {
+            constexpr int t0 = decltype(G)::value * kGrp;
+            u32x4 bh[kGrp], bl[kGrp];
+#pragma unroll
+            for (int q = 0; q < kGrp; ++q) {
+              const int n = min((t0 + q) * 16 + arow, c - 1);
+              const u32x4* bp = reinterpret_cast<const u32x4*>(bs + n * kStride);
+              bh[q] = bp[0];
+              bl[q] = bp[1];
+            }
+#pragma unroll
+            for (int q = 0; q < kGrp; ++q) {
+              acc0[t0 + q] = mfma16x16x32(a0, bh[q], acc0[t0 + q]);
+              acc1[t0 + q] = mfma16x16x32(a1, bh[q], acc1[t0 + q]);
+            }
+#pragma unroll
+            for (int q = 0; q < kGrp; ++q) {
+              acc0[t0 + q] = mfma16x16x32(a0, bl[q], acc0[t0 + q]);
+              acc1[t0 + q] = mfma16x16x32(a1, bl[q], acc1[t0 + q]);
+            }
+          });
         }
         if constexpr (j == kSlot - 1) ring_load(i, min(s / kSlot + kRingP, nslot - 1));
         __builtin_amdgcn_sched_barrier(0);
@@ -558,6 +598,7 @@ void ffn_kernel(FfnArgs a) {
         __syncthreads();
       };
       fetch(0);
+      ring_prologue(Int<1>{}, Int<kRingP>{});
       publish(0);
       __syncthreads();
       const int nround = nfull - nfull % kPhases;
