@@ -402,10 +402,15 @@ void ffn_kernel(FfnArgs a) {
       }
     };
     // Ring slots [FROM, TO) of the prologue.  A CU keeps only so many loads
-    // in flight, so at an item's start the loads go out in the order the
-    // first k-step needs them: ring slot 0, then the first chunk of
-    // activations, then the rest of the ring (the publish of that chunk then
-    // waits for the activations and the slot-0 weights alone).
+    // in flight.  When every item starts with the launch (batches of at most
+    // 64 tokens) and its tokens are known without a load (a routed launch, or
+    // the down projection, whose tokens are its slots), the loads go out in
+    // the order the first k-step needs them: ring slot 0, the first chunk of
+    // activations, then the rest of the ring, and the first publish waits
+    // for the activations and slot 0 alone.  Otherwise (a token list to load
+    // first, or items that start behind others on a busy CU) the whole ring
+    // goes out first (measured: 2% on the mixed 48-layer step at T=128).
+    constexpr bool kEarlyActs = ROUTED || (MODE == kDown && !MULTI);
     auto ring_prologue = [&](auto FROM_, auto TO_) {
 #pragma unroll
       for (int i = decltype(FROM_)::value; i < decltype(TO_)::value; ++i) ring_load(i, min(i, nslot - 1));
@@ -418,10 +423,10 @@ void ffn_kernel(FfnArgs a) {
       __syncthreads();
     };
 
-    // bf16 issues ring slot 0 before the pass shape is chosen; MXFP4's ring
-    // depth depends on the pass shape, so each pass fills its own.
+    // bf16 issues the ring (or its slot 0) before the pass shape is chosen;
+    // MXFP4's ring depth depends on the pass shape, so each pass fills its own.
     if constexpr (FMT == kBf16) {
-      ring_prologue(Int<0>{}, Int<1>{});
+      ring_prologue(Int<0>{}, Int<kEarlyActs ? 1 : kRing>{});
       stage_tokens();
     }
 
@@ -445,7 +450,7 @@ void ffn_kernel(FfnArgs a) {
       constexpr int kGroups = NTB * 16 * 4 * kChunk / kFfnThreads;  // staged 32-byte groups per thread
       static_assert(kGroups * kFfnThreads == NTB * 16 * 4 * kChunk, "groups divide evenly");
       if constexpr (FMT == kMxfp4) {
-        ring_prologue(Int<0>{}, Int<1>{});
+        ring_prologue(Int<0>{}, Int<kEarlyActs ? 1 : kRingP>{});
         stage_tokens();
       }
 
@@ -598,7 +603,7 @@ void ffn_kernel(FfnArgs a) {
         __syncthreads();
       };
       fetch(0);
-      ring_prologue(Int<1>{}, Int<kRingP>{});
+      if constexpr (kEarlyActs) ring_prologue(Int<1>{}, Int<kRingP>{});
       publish(0);
       __syncthreads();
       const int nround = nfull - nfull % kPhases;
