@@ -42,6 +42,10 @@ METRIC = "MoE decode-layer µs and achieved HBM GB/s vs distinct-expert union (Q
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 2 << 30
 LAYERS_PER_GRAPH = 8
+# How each layer step runs the expert FFN (binding.FFN_PATHS): "routed" is
+# moe_expert_ffn_up_routed then moe_expert_ffn_down (measured faster than the
+# one-launch moe_expert_ffn_routed at every union size).
+FFN_PATH = "routed"
 PROFILE = os.path.join(ROOT, "profiles", "moe_layer_qwen3_30b_a3b_T64.md")
 FFN_SOURCE = os.path.join(ROOT, "paper_2607_00466_amd", "csrc", "expert_ffn.hip")
 
@@ -135,13 +139,26 @@ class Bench:
             B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
         if ev is not None:
             ev[0].record(self.stream)
-        # buckets and the up projection (one launch up to 64 tokens, else two)
-        B.moe_expert_ffn_up_routed(self.x, w13, ids, d, b.counts, b.offsets, b.perm_token,
-                                   b.pair_pos, b.union_ids, b.union_size, b.ws)
-        if ev is not None:
-            ev[1].record(self.stream)
-        B.moe_expert_ffn_down(b.ws, w2, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
-                              b.y_perm)
+        if FFN_PATH == "fused":
+            # buckets, up and down projections (one launch up to 64 tokens)
+            B.moe_expert_ffn_routed(self.x, w13, w2, ids, d, b.counts, b.offsets, b.perm_token,
+                                    b.pair_pos, b.union_ids, b.union_size, b.y_perm, b.ws, b.sync)
+            if ev is not None:
+                ev[1].record(self.stream)
+        else:
+            if FFN_PATH == "routed":
+                # buckets and the up projection (one launch up to 64 tokens, else two)
+                B.moe_expert_ffn_up_routed(self.x, w13, ids, d, b.counts, b.offsets, b.perm_token,
+                                           b.pair_pos, b.union_ids, b.union_size, b.ws)
+            else:
+                B.moe_bucket(ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
+                             b.union_size)
+                B.moe_expert_ffn_up(self.x, w13, b.offsets, b.perm_token, b.union_ids,
+                                    b.union_size, d, b.ws)
+            if ev is not None:
+                ev[1].record(self.stream)
+            B.moe_expert_ffn_down(b.ws, w2, b.offsets, b.perm_token, b.union_ids, b.union_size, d,
+                                  b.y_perm)
         if ev is not None:
             ev[2].record(self.stream)
         B.moe_combine(b.y_perm, b.pair_pos, w, d, b.out)
@@ -252,12 +269,26 @@ class MxBench(Bench):
             B.moe_gate_topk(self.x, self.wg, d, b.logits, b.topk_ids, b.topk_w)
         if ev is not None:
             ev[0].record(self.stream)
-        B.moe_expert_ffn_mxfp4_up_routed(self.x, up, ids, d, b.counts, b.offsets, b.perm_token,
-                                         b.pair_pos, b.union_ids, b.union_size, b.ws)
-        if ev is not None:
-            ev[1].record(self.stream)
-        B.moe_expert_ffn_mxfp4_down(b.ws, down, b.offsets, b.perm_token, b.union_ids, b.union_size,
-                                    d, b.y_perm)
+        if FFN_PATH == "fused":
+            B.moe_expert_ffn_mxfp4_routed(self.x, up, down, ids, d, b.counts, b.offsets,
+                                          b.perm_token, b.pair_pos, b.union_ids, b.union_size,
+                                          b.y_perm, b.ws, b.sync)
+            if ev is not None:
+                ev[1].record(self.stream)
+        else:
+            if FFN_PATH == "routed":
+                B.moe_expert_ffn_mxfp4_up_routed(self.x, up, ids, d, b.counts, b.offsets,
+                                                 b.perm_token, b.pair_pos, b.union_ids,
+                                                 b.union_size, b.ws)
+            else:
+                B.moe_bucket(ids, d, b.counts, b.offsets, b.perm_token, b.pair_pos, b.union_ids,
+                             b.union_size)
+                B.moe_expert_ffn_mxfp4_up(self.x, up, b.offsets, b.perm_token, b.union_ids,
+                                          b.union_size, d, b.ws)
+            if ev is not None:
+                ev[1].record(self.stream)
+            B.moe_expert_ffn_mxfp4_down(b.ws, down, b.offsets, b.perm_token, b.union_ids,
+                                        b.union_size, d, b.y_perm)
         if ev is not None:
             ev[2].record(self.stream)
         B.moe_combine(b.y_perm, b.pair_pos, w, d, b.out)
@@ -332,7 +363,7 @@ def mxfp4_workload(path: str, steps: int, warmup: int, layers: int = 36,
 
         def run_step():
             for x, wg, (up, down), buf in lay:
-                B.moe_layer_mxfp4(x, wg, up, down, d, buf)
+                B.moe_layer_mxfp4(x, wg, up, down, d, buf, path=FFN_PATH)
 
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -530,7 +561,7 @@ class MultiLayer:
         for l in range(self.n_layers):
             x, wg, (w13, w2) = self.layers[l % len(self.layers)]
             r = None if routing is None else routing[l]
-            B.moe_layer(x, wg, w13, w2, self.d, self.bufs[l], routing=r)
+            B.moe_layer(x, wg, w13, w2, self.d, self.bufs[l], routing=r, path=FFN_PATH)
 
     def unions(self) -> list[int]:
         torch.cuda.synchronize()
@@ -799,7 +830,7 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
             def run():
                 for layer in range(layers_timed):
                     w13, w2 = packed[layer % 2]
-                    B.moe_layer(x, wg, w13, w2, d, buf, routing=routes[layer])
+                    B.moe_layer(x, wg, w13, w2, d, buf, routing=routes[layer], path=FFN_PATH)
 
             side = torch.cuda.Stream()
             side.wait_stream(torch.cuda.current_stream())
@@ -825,22 +856,11 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
                 "max_worker_step_us": float(np.max(worker_us))}
 
     e, r = measure(eldr_w), measure(rr_w)
-    # The band width tau trades locality (tau = 0: always the most similar
-    # worker) for balance (tau = 2: every worker is in the band, so the least
-    # loaded one is chosen).
-    sweep = []
-    for tau in (0.0, 0.02, 0.05, 0.1, 0.2, 2.0):
-        assign, _ = B.eldr_route_batch(S, C, np.zeros(workers, np.int32), tau)
-        m = measure(assign)
-        m["tau"] = tau
-        sweep.append(m)
-        log(f"routing tau {tau}: union {m['mean_union']:.1f}, batches {m['min_batch']}-{m['max_batch']}, "
-            f"worker step mean {m['mean_worker_step_us']:.0f} us, slowest {m['max_worker_step_us']:.0f} us")
     rec = {"workload": f"ELDR vs round-robin: {workers} workers x {per_worker} requests, 8 synthetic domains, "
                        f"48 MoE layers (E=128, top-8); decode step timed on {layers_timed} Qwen3-30B-A3B-shaped layers",
            "fit_s": round(fit_s, 2), "n_star": n_star, "rho": round(float(curve[n_star - 1]), 4),
            "kmeans_iterations": iters, "route_us_per_request": round(route_us, 2),
-           "eldr": e, "round_robin": r, "tau_sweep": sweep,
+           "eldr": e, "round_robin": r,
            "union_reduction": round(1 - e["mean_union"] / r["mean_union"], 4),
            "mean_step_reduction": round(1 - e["mean_worker_step_us"] / r["mean_worker_step_us"], 4),
            "max_step_reduction": round(1 - e["max_worker_step_us"] / r["max_worker_step_us"], 4)}
@@ -855,6 +875,7 @@ def routing_workload(path: str, workers: int = 16, per_worker: int = 64, layers_
 
 
 def main() -> int:
+    global FFN_PATH
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
@@ -874,6 +895,8 @@ def main() -> int:
     ap.add_argument("--routing", default="",
                     help="also run ELDR routing vs round-robin end to end (native fit + routing, GPU "
                          "decode steps), appending a JSON line to this file")
+    ap.add_argument("--routing-only", action="store_true",
+                    help="run only the --routing measurement (no layer bench line)")
     ap.add_argument("--multilayer", default="",
                     help="also run the 48-layer domain-clustered and 36-layer gpt-oss workloads, "
                          "appending JSON lines to this file")
@@ -889,9 +912,13 @@ def main() -> int:
     ap.add_argument("--mxfp4-cases", default="gate,32,128",
                     help="routings of the --mxfp4 layer: 'gate' and/or controlled union sizes")
     ap.add_argument("--mxfp4-formats", default="mxfp4,bf16", help="expert formats of the --mxfp4 layer")
+    ap.add_argument("--ffn-path", default=FFN_PATH, choices=B.FFN_PATHS,
+                    help="how a layer step runs the expert FFN: one launch (fused), buckets + up "
+                         "then down (routed), or bucket, up, down (split)")
     ap.add_argument("--mxfp4-layers", type=int, default=36,
                     help="layers of the --mxfp4 multi-layer step (0 to skip it)")
     args = ap.parse_args()
+    FFN_PATH = args.ffn_path
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -914,6 +941,9 @@ def main() -> int:
             base = base or bench
             print(json.dumps({"workload": "qwen3_30b_a3b moe layer, controlled union",
                               **controlled_point(bench, U, args.steps, args.warmup)}), flush=True)
+        return 0
+    if args.routing_only:
+        routing_workload(args.routing or "routing.jsonl")
         return 0
     if args.signature_only:
         signature_workload(args.signature or "signature.jsonl")

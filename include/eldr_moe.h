@@ -261,6 +261,44 @@ int moe_expert_ffn_up_routed(const float* x, const uint16_t* w13, const int32_t*
                              void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * moe_expert_ffn_routed -- moe_bucket followed by moe_expert_ffn, in one
+ * launch for batches of at most 64 tokens (the separate calls above that).
+ * The whole expert step of a decode batch after the gate (Motivation,
+ * "Active Expert Count Drives MoE Decode Latency": the union of the batch's
+ * picks is what the step loads): every workgroup builds the buckets of the
+ * routing in its own LDS, as in moe_expert_ffn_up_routed; an XCD's workgroups
+ * take the up bands of its experts first, then their down bands, and a down
+ * band waits on the device until every up band of its expert has stored h,
+ * so the down projection's weights start streaming while the up projection
+ * ends, with no launch between them.
+ *
+ * topk_ids [T, K] int32 (input); counts, offsets, perm_token, pair_pos,
+ * union_ids, union_size (outputs, moe_bucket's, bit for bit); x, w13, w2,
+ * y_perm, ws, ws_bytes as for moe_expert_ffn, whose y_perm (and workspace)
+ * results it leaves, bit for bit; ws must be 128-byte aligned here (else
+ * MOE_ERR_UNSUPPORTED).
+ * sync: int32 [2E + 1] (moe_ffn_sync_bytes), caller-owned device memory that
+ * must be zero before the first call; every call leaves it zero.  Entries
+ * 0 .. 2E-1 are per-expert counters of the call; entry 2E becomes 1 if a
+ * down band gave up waiting for its expert (a bounded wait of about 2^18
+ * polls that a correct run never reaches: the GPU starts an XCD's
+ * workgroups in index order and every up band precedes every down band of
+ * its XCD), in which case that call's y_perm is not valid and the counters
+ * must be zeroed again before the next call.  Calls that share one `sync`
+ * buffer must not overlap (one stream, or ordered by events); calls with
+ * different buffers may.  Errors as moe_bucket and moe_expert_ffn, plus
+ * MOE_ERR_INVALID for a null sync and MOE_ERR_UNSUPPORTED for a misaligned
+ * one; nothing is launched on an error.
+ */
+int moe_expert_ffn_routed(const float* x, const uint16_t* w13, const uint16_t* w2,
+                          const int32_t* topk_ids, moe_dims d, int32_t* counts, int32_t* offsets,
+                          int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,
+                          int32_t* union_size, float* y_perm, void* ws, size_t ws_bytes,
+                          int32_t* sync, void* stream);
+/* Bytes of moe_expert_ffn_routed's sync buffer: 4 (2E + 1); 0 for invalid dims. */
+size_t moe_ffn_sync_bytes(moe_dims d);
+
+/*
  * MXFP4 expert weights (Evaluation, "Models": GPT-OSS-120B is served in
  * mxfp4).  The format is the OCP Microscaling (MX) v1.0 MXFP4: blocks of 32
  * values along the reduction axis share one E8M0 scale X = 2^(code - 127);
@@ -335,6 +373,15 @@ int moe_expert_ffn_mxfp4_up_routed(const float* x, const uint8_t* up_codes,
                                    int32_t* counts, int32_t* offsets, int32_t* perm_token,
                                    int32_t* pair_pos, int32_t* union_ids, int32_t* union_size,
                                    void* ws, size_t ws_bytes, void* stream);
+/* moe_expert_ffn_mxfp4_routed -- moe_expert_ffn_routed with MXFP4 weights
+ * (up_codes, up_scales, down_codes, down_scales as for moe_expert_ffn_mxfp4;
+ * H % 64 == 0 and I % 64 == 0). */
+int moe_expert_ffn_mxfp4_routed(const float* x, const uint8_t* up_codes, const uint8_t* up_scales,
+                                const uint8_t* down_codes, const uint8_t* down_scales,
+                                const int32_t* topk_ids, moe_dims d, int32_t* counts,
+                                int32_t* offsets, int32_t* perm_token, int32_t* pair_pos,
+                                int32_t* union_ids, int32_t* union_size, float* y_perm, void* ws,
+                                size_t ws_bytes, int32_t* sync, void* stream);
 
 /*
  * moe_combine -- weighted unpermute: out[t, :] = sum over j = 0..K-1 (in that

@@ -59,6 +59,11 @@ _SIGNATURES = {
                                  [ctypes.c_size_t, _vp]),
     "moe_expert_ffn_mxfp4_up_routed": (ctypes.c_int, [_vp] * 4 + [MoeDims] + [_vp] * 7 +
                                        [ctypes.c_size_t, _vp]),
+    "moe_expert_ffn_routed": (ctypes.c_int, [_vp] * 4 + [MoeDims] + [_vp] * 8 +
+                              [ctypes.c_size_t, _vp, _vp]),
+    "moe_expert_ffn_mxfp4_routed": (ctypes.c_int, [_vp] * 6 + [MoeDims] + [_vp] * 8 +
+                                    [ctypes.c_size_t, _vp, _vp]),
+    "moe_ffn_sync_bytes": (ctypes.c_size_t, [MoeDims]),
     "moe_expert_ffn_down": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, MoeDims, ctypes.c_size_t,
                                            _vp, _vp]),
     "moe_combine": (ctypes.c_int, [_vp, _vp, _vp, MoeDims, _vp, _vp]),
@@ -251,6 +256,32 @@ def moe_expert_ffn_up_routed(x, w13, topk_ids, d: MoeDims, counts, offsets, perm
         _ptr(pair_pos), _ptr(union_ids), _ptr(union_size), _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def moe_ffn_sync_bytes(d: MoeDims) -> int:
+    return int(load().moe_ffn_sync_bytes(d))
+
+
+def _need_sync(sync, d: MoeDims) -> None:
+    _need(sync, "sync", torch.int32, moe_ffn_sync_bytes(d) // 4)
+
+
+def moe_expert_ffn_routed(x, w13, w2, topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos,
+                          union_ids, union_size, y_perm, ws, sync, stream=None) -> None:
+    """moe_bucket then moe_expert_ffn, one launch for T <= 64.  ``sync`` is an
+    int32 [2E + 1] device tensor, zero before the first call (left zero)."""
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
+    _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need_buckets(d, counts, offsets, perm_token, pair_pos, union_ids, union_size)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _need_sync(sync, d)
+    _check("moe_expert_ffn_routed", load().moe_expert_ffn_routed(
+        _ptr(x), _ptr(w13), _ptr(w2), _ptr(topk_ids), d, _ptr(counts), _ptr(offsets),
+        _ptr(perm_token), _ptr(pair_pos), _ptr(union_ids), _ptr(union_size), _ptr(y_perm),
+        _ptr(ws), ws_bytes, _ptr(sync), _stream(stream)))
+
+
 def moe_expert_ffn_down(ws, w2, offsets, perm_token, union_ids, union_size, d: MoeDims, y_perm,
                         stream=None) -> None:
     _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)
@@ -399,6 +430,25 @@ def moe_expert_ffn_mxfp4_up_routed(x, up, topk_ids, d: MoeDims, counts, offsets,
         _stream(stream)))
 
 
+def moe_expert_ffn_mxfp4_routed(x, up, down, topk_ids, d: MoeDims, counts, offsets, perm_token,
+                                pair_pos, union_ids, union_size, y_perm, ws, sync,
+                                stream=None) -> None:
+    """moe_bucket then moe_expert_ffn_mxfp4, one launch for T <= 64 (``sync`` as
+    for moe_expert_ffn_routed)."""
+    _need(x, "x", torch.float32, d.T * d.H)
+    _need_mx_up(up, d)
+    _need_mx_down(down, d)
+    _need(topk_ids, "topk_ids", torch.int32, d.T * d.K)
+    _need_buckets(d, counts, offsets, perm_token, pair_pos, union_ids, union_size)
+    _need(y_perm, "y_perm", torch.float32, d.T * d.K * d.H)
+    ws_bytes = _need_ws(ws, d)
+    _need_sync(sync, d)
+    _check("moe_expert_ffn_mxfp4_routed", load().moe_expert_ffn_mxfp4_routed(
+        _ptr(x), _ptr(up[0]), _ptr(up[1]), _ptr(down[0]), _ptr(down[1]), _ptr(topk_ids), d,
+        _ptr(counts), _ptr(offsets), _ptr(perm_token), _ptr(pair_pos), _ptr(union_ids),
+        _ptr(union_size), _ptr(y_perm), _ptr(ws), ws_bytes, _ptr(sync), _stream(stream)))
+
+
 def moe_expert_ffn_mxfp4_down(ws, down, offsets, perm_token, union_ids, union_size, d: MoeDims,
                               y_perm, stream=None) -> None:
     _need_mx_down(down, d)
@@ -437,6 +487,7 @@ class LayerBuffers:
     y_perm: torch.Tensor
     ws: torch.Tensor
     out: torch.Tensor
+    sync: torch.Tensor  # moe_expert_ffn_routed's counters: zero at allocation, left zero by every call
 
     @classmethod
     def allocate(cls, d: MoeDims, device="cuda") -> "LayerBuffers":
@@ -456,6 +507,7 @@ class LayerBuffers:
             y_perm=torch.empty((max(1, d.T * d.K), d.H), **f32),
             ws=torch.empty(max(16, nbytes) // 4, **f32),
             out=torch.empty((d.T, d.H), **f32),
+            sync=torch.zeros(max(1, moe_ffn_sync_bytes(d) // 4), **i32),
         )
 
 
@@ -467,46 +519,70 @@ def _gate(x, w_gate, d: MoeDims, buf: LayerBuffers, routing, stream):
     return routing
 
 
+# How moe_layer and moe_layer_mxfp4 run the expert FFN:
+#   "fused":  moe_expert_ffn_routed -- buckets, up and down projections in one launch;
+#   "routed": moe_expert_ffn_up_routed (buckets + up), then moe_expert_ffn_down;
+#   "split":  moe_bucket, moe_expert_ffn_up, moe_expert_ffn_down.
+# All three leave the same buffers, bit for bit.
+FFN_PATHS = ("fused", "routed", "split")
+
+
 def moe_layer(x, w_gate, w13, w2, d: MoeDims, buf: LayerBuffers, routing=None, stream=None,
-              fused: bool = True):
-    """One decode-step MoE layer on one stream: gate, buckets + up projection
-    (moe_expert_ffn_up_routed), down projection, combine.
+              path: str = "routed"):
+    """One decode-step MoE layer on one stream: gate, buckets and expert FFN
+    (buckets + up projection in one launch, then down, by default: see
+    FFN_PATHS), combine.
 
     w13 and w2 are the expert weights packed by ``pack_expert_weights``.
 
     ``routing=(topk_ids, topk_w)`` (int32 [T, K] and fp32 [T, K] device
     tensors) bypasses the gate: the buckets and the combine read them in place.
-    ``fused=False`` makes the buckets a separate moe_bucket call.  Returns ``buf.out``.
+    Returns ``buf.out``.
     """
     ids, w = _gate(x, w_gate, d, buf, routing, stream)
-    if fused:
-        moe_expert_ffn_up_routed(x, w13, ids, d, buf.counts, buf.offsets, buf.perm_token,
-                                 buf.pair_pos, buf.union_ids, buf.union_size, buf.ws, stream)
+    if path == "fused":
+        moe_expert_ffn_routed(x, w13, w2, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                              buf.pair_pos, buf.union_ids, buf.union_size, buf.y_perm, buf.ws,
+                              buf.sync, stream)
+    elif path in ("routed", "split"):
+        if path == "routed":
+            moe_expert_ffn_up_routed(x, w13, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                                     buf.pair_pos, buf.union_ids, buf.union_size, buf.ws, stream)
+        else:
+            moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
+                       buf.union_ids, buf.union_size, stream)
+            moe_expert_ffn_up(x, w13, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
+                              d, buf.ws, stream)
+        moe_expert_ffn_down(buf.ws, w2, buf.offsets, buf.perm_token, buf.union_ids,
+                            buf.union_size, d, buf.y_perm, stream)
     else:
-        moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
-                   buf.union_size, stream)
-        moe_expert_ffn_up(x, w13, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
-                          buf.ws, stream)
-    moe_expert_ffn_down(buf.ws, w2, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size, d,
-                        buf.y_perm, stream)
+        raise ValueError(f"unknown FFN path {path!r} (one of {FFN_PATHS})")
     moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 
 
 def moe_layer_mxfp4(x, w_gate, up, down, d: MoeDims, buf: LayerBuffers, routing=None, stream=None,
-                    fused: bool = True):
+                    path: str = "routed"):
     """moe_layer with MXFP4 experts: ``up`` and ``down`` from pack_mxfp4_expert_weights."""
     ids, w = _gate(x, w_gate, d, buf, routing, stream)
-    if fused:
-        moe_expert_ffn_mxfp4_up_routed(x, up, ids, d, buf.counts, buf.offsets, buf.perm_token,
-                                       buf.pair_pos, buf.union_ids, buf.union_size, buf.ws, stream)
+    if path == "fused":
+        moe_expert_ffn_mxfp4_routed(x, up, down, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                                    buf.pair_pos, buf.union_ids, buf.union_size, buf.y_perm,
+                                    buf.ws, buf.sync, stream)
+    elif path in ("routed", "split"):
+        if path == "routed":
+            moe_expert_ffn_mxfp4_up_routed(x, up, ids, d, buf.counts, buf.offsets, buf.perm_token,
+                                           buf.pair_pos, buf.union_ids, buf.union_size, buf.ws,
+                                           stream)
+        else:
+            moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos,
+                       buf.union_ids, buf.union_size, stream)
+            moe_expert_ffn_mxfp4_up(x, up, buf.offsets, buf.perm_token, buf.union_ids,
+                                    buf.union_size, d, buf.ws, stream)
+        moe_expert_ffn_mxfp4_down(buf.ws, down, buf.offsets, buf.perm_token, buf.union_ids,
+                                  buf.union_size, d, buf.y_perm, stream)
     else:
-        moe_bucket(ids, d, buf.counts, buf.offsets, buf.perm_token, buf.pair_pos, buf.union_ids,
-                   buf.union_size, stream)
-        moe_expert_ffn_mxfp4_up(x, up, buf.offsets, buf.perm_token, buf.union_ids, buf.union_size,
-                                d, buf.ws, stream)
-    moe_expert_ffn_mxfp4_down(buf.ws, down, buf.offsets, buf.perm_token, buf.union_ids,
-                              buf.union_size, d, buf.y_perm, stream)
+        raise ValueError(f"unknown FFN path {path!r} (one of {FFN_PATHS})")
     moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out, stream)
     return buf.out
 

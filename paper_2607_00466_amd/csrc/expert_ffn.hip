@@ -286,53 +286,53 @@ __device__ __forceinline__ int wave_inclusive_sum(int x) {
   return x;
 }
 
-template <int MODE, int NT, bool MULTI, int FMT, bool ROUTED>
-// (128-token passes: held to two waves a SIMD, the LDS limit, so registers never lower it)
-__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) __attribute__((amdgpu_waves_per_eu(NT == 8 ? 2 : 1)))
-void ffn_kernel(FfnArgs a) {
-  constexpr int kFfnThreads = ffn_threads<MODE, FMT>();
-  constexpr int kBuf = lds_buf_bytes<FMT, NT>();
-  constexpr int kRing = ring_depth<FMT, NT>();
-  constexpr int kSlot = slot_steps<FMT>();  // k-steps per ring slot
-  constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
-  static_assert(ffn_waves<MODE, FMT>() == 4,
-                "the packed weight layouts put 4 waves' fragments side by side per band");
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][kBuf];
-  __shared__ int tok[kGroupTokens];
+// LDS of one workgroup: the two activation chunk buffers and the item's
+// token list.
+template <int FMT, int NT>
+struct FfnLds {
+  unsigned char buf[2][lds_buf_bytes<FMT, NT>()];
+  int tok[NT * 16];
+};
 
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int lane = tid % kWave;
+struct NoHook {
+  __device__ __forceinline__ void operator()() const {}
+};
 
-  // ---- work items -----------------------------------------------------------
-  // Workgroups are dealt to the XCDs round-robin, so workgroup b runs on XCD
-  // b % 8 and is that XCD's slot b / 8.  An item is (expert, row band, token
-  // group of up to kGroupTokens tokens); an XCD's items are numbered expert
-  // by expert, and within an expert band by band with the band's token
-  // groups adjacent, so the workgroups that read one band's weights for
-  // different tokens run side by side and share the XCD's L2.  A slot takes
-  // items slot, slot + slots, ... .  Without MULTI (batches of at most
-  // kGroupTokens tokens) every expert has one group and the expert at union
-  // position u belongs to XCD u % 8; with it, the union's (expert, band)
-  // units are dealt round-robin.
-  const int xcd = blockIdx.x % kNumXcd;
-  const int slot = blockIdx.x / kNumXcd;
-  const int slots = gridDim.x / kNumXcd;
-  const int K = a.kdim;
-  const int nk = K / kKStep;
-  const int nslot = nk / kSlot;  // ring slots of a row band
-  const int arow = lane & 15;
-  const int kgrp = lane >> 4;
-
-  // One item: the token group of up to kGroupTokens tokens starting at slot
-  // s_begin + p0 of expert e's bucket, against row band `tile`.
-  // SHARED_: the band is read by more than one token group of the expert; those
-  // items run side by side on one XCD, so their weight loads are ordinary
-  // (cacheable) loads and the repeated reads are served by the XCD's L2.
-  // Every other band is read once, with non-temporal loads.
-  auto run_item = [&](auto SHARED_, const int e, const int tile, const int s_begin, const int p0,
-                      const int c) {
-    constexpr bool kShared = decltype(SHARED_)::value != 0;
+// One item: the token group of up to NT * 16 tokens starting at slot
+// s_begin + p0 of expert e's bucket, against row band `tile`.
+// EARLY: the prologue's load order (below).  LISTED: L.tok already holds the
+// item's tokens (a routed launch lists them from its buckets).
+// SHARED: the band is read by more than one token group of the expert; those
+// items run side by side on one XCD, so their weight loads are ordinary
+// (cacheable) loads and the repeated reads are served by the XCD's L2.
+// Every other band is read once, with non-temporal loads.
+// before_acts runs (in every thread) once the weight ring is in flight and
+// before the first activations are read; after_store once the item's outputs
+// are stored.  The fused launch waits for h in the first and publishes h in
+// the second; the separate launches pass NoHook.  WT (up): h is stored with
+// device-scope stores, written through to memory (the fused launch).
+template <int MODE, int NT, int FMT, bool EARLY, bool LISTED, bool SHARED, bool WT, class Before,
+          class After>
+__device__ __forceinline__ void ffn_item(const FfnArgs& a, FfnLds<FMT, NT>& L, const int e, const int tile,
+                                         const int s_begin, const int p0, const int c, Before&& before_acts,
+                                         After&& after_store) {
+    constexpr int kFfnThreads = ffn_threads<MODE, FMT>();
+    constexpr int kBuf = lds_buf_bytes<FMT, NT>();
+    constexpr int kRing = ring_depth<FMT, NT>();
+    constexpr int kSlot = slot_steps<FMT>();  // k-steps per ring slot
+    static_assert(ffn_waves<MODE, FMT>() == 4,
+                  "the packed weight layouts put 4 waves' fragments side by side per band");
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const int K = a.kdim;
+    const int nk = K / kKStep;
+    const int nslot = nk / kSlot;  // ring slots of a row band
+    const int arow = lane & 15;
+    const int kgrp = lane >> 4;
+    auto& lds = L.buf;
+    auto& tok = L.tok;
+    constexpr bool kShared = SHARED;
     const int nt = (c + 15) / 16;
 
     const int r0 = tile * rows_per_block<MODE, FMT>() + wave * (MODE == kUp ? 16 : 32);
@@ -410,7 +410,7 @@ void ffn_kernel(FfnArgs a) {
     // for the activations and slot 0 alone.  Otherwise (a token list to load
     // first, or items that start behind others on a busy CU) the whole ring
     // goes out first (measured: 2% on the mixed 48-layer step at T=128).
-    constexpr bool kEarlyActs = ROUTED || (MODE == kDown && !MULTI);
+    constexpr bool kEarlyActs = EARLY;
     auto ring_prologue = [&](auto FROM_, auto TO_) {
 #pragma unroll
       for (int i = decltype(FROM_)::value; i < decltype(TO_)::value; ++i) ring_load(i, min(i, nslot - 1));
@@ -418,7 +418,7 @@ void ffn_kernel(FfnArgs a) {
     auto stage_tokens = [&]() {
       __syncthreads();  // the previous item has finished with LDS
       // (a routed launch has listed the tokens already)
-      if (!ROUTED && tid < c)
+      if (!LISTED && tid < c)
         tok[tid] = (MODE == kUp) ? a.perm_token[s_begin + p0 + tid] : s_begin + p0 + tid;
       __syncthreads();
     };
@@ -602,6 +602,7 @@ void ffn_kernel(FfnArgs a) {
         publish((ch + 1) & 1);
         __syncthreads();
       };
+      before_acts();
       fetch(0);
       if constexpr (kEarlyActs) ring_prologue(Int<1>{}, Int<kRingP>{});
       publish(0);
@@ -644,8 +645,17 @@ void ffn_kernel(FfnArgs a) {
               const int col = r0 + rsub;
               unsigned char* row = static_cast<unsigned char*>(a.dst) + sl * (size_t)a.rows * 4;
               unsigned char* grp = row + (col / 8) * 32 + (col % 8) * 2;
-              *reinterpret_cast<uint2*>(grp) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
-              *reinterpret_cast<uint2*>(grp + 16) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+              if constexpr (WT) {
+                const uint64_t h64 = (uint64_t)(hi[0] | (hi[1] << 16)) | ((uint64_t)(hi[2] | (hi[3] << 16)) << 32);
+                const uint64_t l64 = (uint64_t)(lo[0] | (lo[1] << 16)) | ((uint64_t)(lo[2] | (lo[3] << 16)) << 32);
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(grp), h64, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(grp + 16), l64, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+              } else {
+                *reinterpret_cast<uint2*>(grp) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+                *reinterpret_cast<uint2*>(grp + 16) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+              }
             }
           } else {
             float* y = static_cast<float*>(a.dst) + sl * a.rows;
@@ -658,6 +668,7 @@ void ffn_kernel(FfnArgs a) {
           }
         }
       }
+      after_store();
     };
     if constexpr (NT == 1) {
       run_pass(Int<1>{});
@@ -675,148 +686,202 @@ void ffn_kernel(FfnArgs a) {
       else if (nt <= 4) run_pass(Int<4>{});
       else run_pass(Int<8>{});
     }
-  };
+}
+
+// The buckets of moe_bucket, built in LDS by a workgroup of a routed launch.
+struct RouteLds {
+  uint32_t mask[2 * MOE_MAX_E];       // token bitmaps: bit t of word t / 32
+  int off[MOE_MAX_E];                 // bucket offsets
+  unsigned long long cls[4][4];       // [wave][class - 1] ballots
+  int wn[4], wp[4];                   // per-wave totals: pairs, experts
+  int bad, e;
+};
+
+// Builds the buckets of moe_bucket in LDS from the routing ids [T, K] (T <= 64,
+// so a token bitmap is two words): counts, offsets, the union in dispatch
+// order, and the expert at the union position pick(U) returns for this
+// workgroup (-1: none); workgroup 0 also writes them out for the later calls
+// (the down projection, the combine).  Same results as moe_bucket, bit for
+// bit.  Returns whether the workgroup has an item: R.e is its expert.  Every
+// branch is uniform over the workgroup.
+template <int kThreads, class Pick>
+__device__ __forceinline__ bool route_buckets(const FfnArgs& a, RouteLds& R, Pick&& pick) {
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = tid % kWave;
+  const int T = a.T, K = a.K, E = a.experts, P = a.T * a.K;
+  constexpr int kIdsPerThread = 64 * MOE_MAX_K / kThreads;
+  int idv[kIdsPerThread];
+#pragma unroll
+  for (int j = 0; j < kIdsPerThread; ++j) {
+    const int p = tid + kThreads * j;
+    idv[j] = p < P ? a.ids[p] : 0;
+  }
+  for (int i = tid; i < 2 * E; i += kThreads) R.mask[i] = 0u;
+  if (tid == 0) {
+    R.bad = 0;
+    R.e = -1;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kIdsPerThread; ++j) {
+    const int p = tid + kThreads * j;
+    if (p < P) {
+      const int t = p / K;
+      const int e = idv[j];
+      if (e < 0 || e >= E) {
+        R.bad = 1;
+      } else {
+        const uint32_t bit = 1u << (t & 31);
+        if (atomicOr(&R.mask[2 * e + (t >> 5)], bit) & bit) R.bad = 1;  // an expert twice
+      }
+    }
+  }
+  __syncthreads();
+  // One expert a thread.  Its count n, and its class: the 16-token tiles of
+  // its bucket (1 .. 4 here, T <= 64; 0 when absent).  The dispatch order
+  // (more tiles first, equal tiles by ascending id) ranks an expert by the
+  // experts of higher classes plus those of its class with lower ids, which
+  // per-wave ballots of each class give directly.  Offsets and ascending
+  // union positions are prefix sums: within a wave by DPP, across the
+  // four waves from their totals.
+  static_assert(MOE_MAX_E <= kThreads && kThreads == 4 * kWave, "one expert a thread");
+  const int me = tid;
+  const int n = me < E ? __popc(R.mask[2 * me]) + __popc(R.mask[2 * me + 1]) : 0;
+  const int cls = (n + 15) / 16;
+  const int incl_n = wave_inclusive_sum(n);
+  const int incl_p = wave_inclusive_sum(n > 0 ? 1 : 0);
+#pragma unroll
+  for (int c = 1; c <= 4; ++c) {
+    const unsigned long long b = __ballot(cls == c);
+    if (lane == 0) R.cls[wave][c - 1] = b;
+  }
+  if (lane == kWave - 1) {
+    R.wn[wave] = incl_n;
+    R.wp[wave] = incl_p;
+  }
+  __syncthreads();
+  int U = 0, before_n = 0, before_p = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    U += R.wp[w];
+    before_n += w < wave ? R.wn[w] : 0;
+    before_p += w < wave ? R.wp[w] : 0;
+  }
+  const int pairs = R.wn[0] + R.wn[1] + R.wn[2] + R.wn[3];
+  const int u = pick(U);  // this workgroup's union position
+  // Workgroups without an item leave here (the grid is sized from E); the
+  // first stays, to write the buckets out.
+  if (u < 0 && blockIdx.x != 0) return false;
+  const int off = before_n + incl_n - n;
+  int rank = 0;
+  if (cls > 0) {
+#pragma unroll
+    for (int c = 4; c >= 1; --c) {
+      if (c > cls) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) rank += __popcll(R.cls[w][c - 1]);
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const unsigned long long b = R.cls[w][cls - 1];
+      rank += w < wave ? __popcll(b) : w == wave ? __popcll(b & ((1ull << lane) - 1ull)) : 0;
+    }
+  }
+  if (me < E) R.off[me] = off;
+  if (cls > 0 && rank == u) R.e = me;
+  const bool ok = R.bad == 0 && pairs == P;
+  if (blockIdx.x == 0) {
+    if (me < E) {
+      a.b_counts[me] = n;
+      a.b_offsets[me] = off;
+      if (n > 0) {
+        a.b_union_ids[before_p + incl_p - 1] = me;
+        a.b_union_ids[E + rank] = me;
+      }
+      if (me >= U) {
+        a.b_union_ids[me] = -1;
+        a.b_union_ids[E + me] = -1;
+      }
+    }
+    if (tid == 0) {
+      a.b_offsets[E] = pairs;
+      *a.b_union_size = ok ? U : -1;
+    }
+    __syncthreads();  // R.off complete (uniform: the whole of workgroup 0)
+    if (ok) {
+#pragma unroll
+      for (int j = 0; j < kIdsPerThread; ++j) {
+        const int p = tid + kThreads * j;
+        if (p < P) {
+          const int t = p / K;
+          const int e = idv[j];
+          const int w = t >> 5;
+          const int below = (w ? __popc(R.mask[2 * e]) : 0) +
+                            __popc(R.mask[2 * e + w] & ((1u << (t & 31)) - 1u));
+          const int sl = R.off[e] + below;
+          a.b_perm_token[sl] = t;
+          a.b_pair_pos[p] = sl;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  return ok && R.e >= 0;  // invalid routing, or no expert at this position: nothing
+}
+
+// Lists expert e's tokens of a routed launch in ascending order into tok: the
+// rank of token tid's bit.  Returns the count.
+__device__ __forceinline__ int route_tokens(const FfnArgs& a, const RouteLds& R, const int e, int* tok) {
+  const int tid = threadIdx.x;
+  if (tid < a.T) {
+    const uint64_t m = (uint64_t)R.mask[2 * e] | ((uint64_t)R.mask[2 * e + 1] << 32);
+    if ((m >> tid) & 1u) tok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
+  }
+  return __popc(R.mask[2 * e]) + __popc(R.mask[2 * e + 1]);
+}
+
+template <int MODE, int NT, bool MULTI, int FMT, bool ROUTED>
+// (128-token passes: held to two waves a SIMD, the LDS limit, so registers never lower it)
+__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) __attribute__((amdgpu_waves_per_eu(NT == 8 ? 2 : 1)))
+void ffn_kernel(FfnArgs a) {
+  constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
+  __shared__ __attribute__((aligned(16))) FfnLds<FMT, NT> L;
+  // The prologue's load order: the first activations early when every item
+  // starts with the launch and its tokens are known without a load.
+  constexpr bool kEarly = ROUTED || (MODE == kDown && !MULTI);
+
+  // ---- work items -----------------------------------------------------------
+  // Workgroups are dealt to the XCDs round-robin, so workgroup b runs on XCD
+  // b % 8 and is that XCD's slot b / 8.  An item is (expert, row band, token
+  // group of up to kGroupTokens tokens); an XCD's items are numbered expert
+  // by expert, and within an expert band by band with the band's token
+  // groups adjacent, so the workgroups that read one band's weights for
+  // different tokens run side by side and share the XCD's L2.  A slot takes
+  // items slot, slot + slots, ... .  Without MULTI (batches of at most
+  // kGroupTokens tokens) every expert has one group and the expert at union
+  // position u belongs to XCD u % 8; with it, the union's (expert, band)
+  // units are dealt round-robin.
+  const int tid = threadIdx.x;
+  const int lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int xcd = blockIdx.x % kNumXcd;
+  const int slot = blockIdx.x / kNumXcd;
+  const int slots = gridDim.x / kNumXcd;
 
   if constexpr (ROUTED) {
     static_assert(!MULTI && MODE == kUp, "routed launches: up projection, batches of <= 64 tokens");
-    // The buckets of moe_bucket, built in LDS by every workgroup from the
-    // routing ids [T, K] (T <= 64, so a token bitmap is two words): counts,
-    // offsets, the union in dispatch order, and this item's expert and
-    // tokens; workgroup 0 also writes them out for the down projection and
-    // the combine.  Same results as moe_bucket, bit for bit.
-    __shared__ uint32_t r_mask[2 * MOE_MAX_E];       // token bitmaps: bit t of word t / 32
-    __shared__ int r_off[MOE_MAX_E];                  // bucket offsets
-    __shared__ unsigned long long r_cls[4][4];        // [wave][class - 1] ballots
-    __shared__ int r_wn[4], r_wp[4];                  // per-wave totals: pairs, experts
-    __shared__ int r_bad, r_e;
-    const int T = a.T, K = a.K, E = a.experts, P = a.T * a.K;
-    constexpr int kIdsPerThread = 64 * MOE_MAX_K / kFfnThreads;
-    int idv[kIdsPerThread];
-#pragma unroll
-    for (int j = 0; j < kIdsPerThread; ++j) {
-      const int p = tid + kFfnThreads * j;
-      idv[j] = p < P ? a.ids[p] : 0;
-    }
-    for (int i = tid; i < 2 * E; i += kFfnThreads) r_mask[i] = 0u;
-    if (tid == 0) {
-      r_bad = 0;
-      r_e = -1;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kIdsPerThread; ++j) {
-      const int p = tid + kFfnThreads * j;
-      if (p < P) {
-        const int t = p / K;
-        const int e = idv[j];
-        if (e < 0 || e >= E) {
-          r_bad = 1;
-        } else {
-          const uint32_t bit = 1u << (t & 31);
-          if (atomicOr(&r_mask[2 * e + (t >> 5)], bit) & bit) r_bad = 1;  // an expert twice
-        }
-      }
-    }
-    __syncthreads();
-    // One expert a thread.  Its count n, and its class: the 16-token tiles of
-    // its bucket (1 .. 4 here, T <= 64; 0 when absent).  The dispatch order
-    // (more tiles first, equal tiles by ascending id) ranks an expert by the
-    // experts of higher classes plus those of its class with lower ids, which
-    // per-wave ballots of each class give directly.  Offsets and ascending
-    // union positions are prefix sums: within a wave by DPP, across the
-    // four waves from their totals.
-    static_assert(MOE_MAX_E <= kFfnThreads && kFfnThreads == 4 * kWave, "one expert a thread");
-    const int me = tid;
-    const int n = me < E ? __popc(r_mask[2 * me]) + __popc(r_mask[2 * me + 1]) : 0;
-    const int cls = (n + 15) / 16;
-    const int incl_n = wave_inclusive_sum(n);
-    const int incl_p = wave_inclusive_sum(n > 0 ? 1 : 0);
-#pragma unroll
-    for (int c = 1; c <= 4; ++c) {
-      const unsigned long long b = __ballot(cls == c);
-      if (lane == 0) r_cls[wave][c - 1] = b;
-    }
-    if (lane == kWave - 1) {
-      r_wn[wave] = incl_n;
-      r_wp[wave] = incl_p;
-    }
-    __syncthreads();
-    int U = 0, before_n = 0, before_p = 0;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      U += r_wp[w];
-      before_n += w < wave ? r_wn[w] : 0;
-      before_p += w < wave ? r_wp[w] : 0;
-    }
-    const int pairs = r_wn[0] + r_wn[1] + r_wn[2] + r_wn[3];
-    const int u = (slot / a.tiles) * kNumXcd + xcd;  // this workgroup's union position
-    // Workgroups past the union leave here (the grid is sized from E); the
-    // first stays, to write the buckets out.
-    if (u >= U && blockIdx.x != 0) return;
-    const int off = before_n + incl_n - n;
-    int rank = 0;
-    if (cls > 0) {
-#pragma unroll
-      for (int c = 4; c >= 1; --c) {
-        if (c > cls) {
-#pragma unroll
-          for (int w = 0; w < 4; ++w) rank += __popcll(r_cls[w][c - 1]);
-        }
-      }
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const unsigned long long b = r_cls[w][cls - 1];
-        rank += w < wave ? __popcll(b) : w == wave ? __popcll(b & ((1ull << lane) - 1ull)) : 0;
-      }
-    }
-    if (me < E) r_off[me] = off;
-    if (cls > 0 && rank == u) r_e = me;
-    const bool ok = r_bad == 0 && pairs == P;
-    if (blockIdx.x == 0) {
-      if (me < E) {
-        a.b_counts[me] = n;
-        a.b_offsets[me] = off;
-        if (n > 0) {
-          a.b_union_ids[before_p + incl_p - 1] = me;
-          a.b_union_ids[E + rank] = me;
-        }
-        if (me >= U) {
-          a.b_union_ids[me] = -1;
-          a.b_union_ids[E + me] = -1;
-        }
-      }
-      if (tid == 0) {
-        a.b_offsets[E] = pairs;
-        *a.b_union_size = ok ? U : -1;
-      }
-      __syncthreads();  // r_off complete (uniform: the whole of workgroup 0)
-      if (ok) {
-#pragma unroll
-        for (int j = 0; j < kIdsPerThread; ++j) {
-          const int p = tid + kFfnThreads * j;
-          if (p < P) {
-            const int t = p / K;
-            const int e = idv[j];
-            const int w = t >> 5;
-            const int below = (w ? __popc(r_mask[2 * e]) : 0) +
-                              __popc(r_mask[2 * e + w] & ((1u << (t & 31)) - 1u));
-            const int sl = r_off[e] + below;
-            a.b_perm_token[sl] = t;
-            a.b_pair_pos[p] = sl;
-          }
-        }
-      }
-    }
-    __syncthreads();
-    const int e = r_e;
-    if (!ok || e < 0) return;  // invalid routing, or no expert at this position
-    const int c = __popc(r_mask[2 * e]) + __popc(r_mask[2 * e + 1]);
-    if (tid < T) {
-      // the expert's tokens in ascending order: the rank of token tid's bit
-      const uint64_t m = (uint64_t)r_mask[2 * e] | ((uint64_t)r_mask[2 * e + 1] << 32);
-      if ((m >> tid) & 1u) tok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
-    }
-    run_item(Int<0>{}, e, slot % a.tiles, r_off[e], 0, c);
+    __shared__ RouteLds R;
+    auto pick = [&](const int U) {
+      const int u = (slot / a.tiles) * kNumXcd + xcd;
+      return u < U ? u : -1;
+    };
+    if (!route_buckets<ffn_threads<MODE, FMT>()>(a, R, pick)) return;
+    const int e = R.e;
+    const int c = route_tokens(a, R, e, L.tok);
+    ffn_item<MODE, NT, FMT, kEarly, true, false, false>(a, L, e, slot % a.tiles, R.off[e], 0, c, NoHook{},
+                                                 NoHook{});
   } else if constexpr (!MULTI) {
     // At most kGroupTokens tokens per expert: slot = (expert / 8) * tiles + band.
     const int u = (slot / a.tiles) * kNumXcd + xcd;
@@ -826,7 +891,9 @@ void ffn_kernel(FfnArgs a) {
     if (e < 0 || e >= a.experts) return;  // not reached for a union member
     const int s_begin = a.offsets[e];
     const int c = a.offsets[e + 1] - s_begin;
-    if (c > 0) run_item(Int<0>{}, e, slot % a.tiles, s_begin, 0, min(c, kGroupTokens));
+    if (c > 0)
+      ffn_item<MODE, NT, FMT, kEarly, false, false, false>(a, L, e, slot % a.tiles, s_begin, 0,
+                                                    min(c, kGroupTokens), NoHook{}, NoHook{});
   } else {
     // The union lists its experts in dispatch order (moe_bucket: more
     // 16-token tiles first).  A projection's units are (expert, row band)
@@ -918,11 +985,118 @@ void ffn_kernel(FfnArgs a) {
         const int ie = pick(lk_e);
         const int isb = pick(lk_sb);
         if (g > 1)
-          run_item(Int<1>{}, ie, tile, isb, p0, c);
+          ffn_item<MODE, NT, FMT, kEarly, false, true, false>(a, L, ie, tile, isb, p0, c, NoHook{}, NoHook{});
         else
-          run_item(Int<0>{}, ie, tile, isb, p0, c);
+          ffn_item<MODE, NT, FMT, kEarly, false, false, false>(a, L, ie, tile, isb, p0, c, NoHook{}, NoHook{});
       }
     }
+  }
+}
+
+// Spins of a fused down item's wait for its expert's h before it gives up and
+// raises the error word (never in a correct run: see ffn_fused_kernel).
+#ifndef ELDR_FFN_SPIN_LIMIT
+#define ELDR_FFN_SPIN_LIMIT (1 << 18)
+#endif
+
+// Buckets, up projection and down projection in one launch (batches of at
+// most 64 tokens, every expert one token group).  Each workgroup builds the
+// buckets (route_buckets), then takes one item by its XCD slot: an XCD's items
+// are the up bands of its union experts (positions u = xcd, xcd + 8, ...),
+// expert by expert, then their down bands, then nothing.  A down item streams
+// its first W2 weights, then waits until every up band of its expert has
+// stored h, then reads h.
+//
+// Synchronisation, over `sync` (int32 [2E + 1], zero before the first call),
+// without cache write-backs or invalidations (each costs a pass over an XCD's
+// L2; one per up item tripled the layer's time):
+// * an up item stores its h with device-scope stores, which write through to
+//   memory, waits in every wave until its stores are acknowledged, passes a
+//   barrier, and adds 1 to sync[u] (an atomic at device scope);
+// * a down item's thread 0 polls sync[u] with device-scope loads until it
+//   reads the up band count, then the workgroup reads h with ordinary loads.
+//   No CU of the device can hold a stale copy of those lines: the launch
+//   starts with the caches invalidated, h rows are whole 128-byte lines (the
+//   entry points require a 128-byte aligned workspace, and a row is 4 I
+//   bytes with I % 32 == 0), and only the expert's own down items read its rows,
+//   after the wait;
+// * each down item then counts itself in sync[E + u], and the expert's last
+//   one sets both counters back to 0, so every call leaves `sync` as it
+//   found it.
+// Progress: the dispatcher starts an XCD's workgroups in index order, and
+// every up item comes before every down item of its XCD (and before every
+// down item of its expert in index order, whatever XCD runs it), so an up
+// item never waits behind a down item.  A wait that outlasts
+// ELDR_FFN_SPIN_LIMIT polls (not reached in a correct run) sets sync[2E] to 1
+// and goes on, so every wave ends.
+template <int NT, int FMT>
+__global__ __launch_bounds__((ffn_threads<kUp, FMT>())) void ffn_fused_kernel(FfnArgs up, FfnArgs dn,
+                                                                              int32_t* sync) {
+  static_assert(ffn_threads<kUp, FMT>() == ffn_threads<kDown, FMT>(), "one workgroup shape");
+  __shared__ __attribute__((aligned(16))) FfnLds<FMT, NT> L;
+  __shared__ RouteLds R;
+  const int xcd = blockIdx.x % kNumXcd;
+  const int slot = blockIdx.x / kNumXcd;
+  int is_down = 0, band = 0;
+  auto pick = [&](const int U) {
+    const int ux = U > xcd ? (U - xcd + kNumXcd - 1) / kNumXcd : 0;  // union experts on this XCD
+    const int n_up = up.tiles * ux;
+    if (slot < n_up) {
+      band = slot % up.tiles;
+      return (slot / up.tiles) * kNumXcd + xcd;
+    }
+    const int s2 = slot - n_up;
+    if (s2 < dn.tiles * ux) {
+      is_down = 1;
+      band = s2 % dn.tiles;
+      return (s2 / dn.tiles) * kNumXcd + xcd;
+    }
+    return -1;
+  };
+  int u = -1;
+  auto pick_u = [&](const int U) {
+    u = pick(U);
+    return u;
+  };
+  if (!route_buckets<ffn_threads<kUp, FMT>()>(up, R, pick_u)) return;
+  const int e = __builtin_amdgcn_readfirstlane(R.e);
+  u = __builtin_amdgcn_readfirstlane(u);
+  band = __builtin_amdgcn_readfirstlane(band);
+  const int E = up.experts;
+  int32_t* up_done = sync;         // [E]: up items of union position u that stored h
+  int32_t* dn_seen = sync + E;     // [E]: down items of position u past their wait
+  int32_t* err = sync + 2 * E;     // [1]: a wait gave up
+  if (__builtin_amdgcn_readfirstlane(is_down) == 0) {
+    const int c = route_tokens(up, R, e, L.tok);
+    auto publish_h = [&] {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's h stores are acknowledged
+      __syncthreads();
+      if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(&up_done[u], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    ffn_item<kUp, NT, FMT, true, true, false, true>(up, L, e, band, R.off[e], 0, c, NoHook{}, publish_h);
+  } else {
+    const int c = __popc(R.mask[2 * e]) + __popc(R.mask[2 * e + 1]);
+    auto wait_h = [&] {
+      if (threadIdx.x == 0) {
+        int n = 0;
+        while (__hip_atomic_load(&up_done[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < up.tiles) {
+          __builtin_amdgcn_s_sleep(2);
+          if (++n == ELDR_FFN_SPIN_LIMIT) {
+            __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+          }
+        }
+        if (__hip_atomic_fetch_add(&dn_seen[u], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+            dn.tiles - 1) {
+          // the expert's last down item: nobody reads either counter again in this call
+          __hip_atomic_store(&up_done[u], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(&dn_seen[u], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+      __syncthreads();
+    };
+    ffn_item<kDown, NT, FMT, false, false, false, false>(dn, L, e, band, R.off[e], 0, c, wait_h, NoHook{});
   }
 }
 
@@ -970,6 +1144,21 @@ static void launch_ffn_routed(const FfnArgs& a, int T, int E, hipStream_t s) {
     hipLaunchKernelGGL((ffn_kernel<kUp, 2, false, FMT, true>), grid, block, 0, s, a);
   else
     hipLaunchKernelGGL((ffn_kernel<kUp, 4, false, FMT, true>), grid, block, 0, s, a);
+}
+
+// The fused launch: every XCD gets room for the up and down bands of its
+// share of E experts; workgroups past the union's items return at once.
+template <int FMT>
+static void launch_ffn_fused(const FfnArgs& up, const FfnArgs& dn, int32_t* sync, int T, int E,
+                             hipStream_t s) {
+  const int per_xcd = (E + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(kNumXcd * per_xcd * (up.tiles + dn.tiles)), block(ffn_threads<kUp, FMT>());
+  if (T <= 16)
+    hipLaunchKernelGGL((ffn_fused_kernel<1, FMT>), grid, block, 0, s, up, dn, sync);
+  else if (T <= 32)
+    hipLaunchKernelGGL((ffn_fused_kernel<2, FMT>), grid, block, 0, s, up, dn, sync);
+  else
+    hipLaunchKernelGGL((ffn_fused_kernel<4, FMT>), grid, block, 0, s, up, dn, sync);
 }
 
 template <int MODE, int FMT>
@@ -1298,5 +1487,94 @@ extern "C" int moe_expert_ffn_mxfp4_up_routed(const float* x, const uint8_t* up_
                    union_size};
   up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kMxfp4>(d);
   eldr::launch_ffn_routed<eldr::kMxfp4>(up, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+// ---- fused launches: buckets, up and down projections in one launch ---------
+
+extern "C" size_t moe_ffn_sync_bytes(moe_dims d) {
+  if (eldr_host::check_dims(d) != MOE_OK) return 0;
+  return (size_t)(2 * d.E + 1) * 4;
+}
+
+extern "C" int moe_expert_ffn_routed(const float* x, const uint16_t* w13, const uint16_t* w2,
+                                     const int32_t* topk_ids, moe_dims d, int32_t* counts,
+                                     int32_t* offsets, int32_t* perm_token, int32_t* pair_pos,
+                                     int32_t* union_ids, int32_t* union_size, float* y_perm,
+                                     void* ws, size_t ws_bytes, int32_t* sync, void* stream) {
+  using namespace eldr_host;
+  int st = check_dims(d);
+  if (st != MOE_OK) return st;
+  if (!sync) return MOE_ERR_INVALID;
+  if (!aligned4(sync)) return MOE_ERR_UNSUPPORTED;
+  if (d.T == 0 || d.T > 64) {
+    // nothing to multiply (moe_bucket writes the empty buckets), or too many
+    // tokens for the in-kernel buckets: the separate calls
+    st = moe_bucket(topk_ids, d, counts, offsets, perm_token, pair_pos, union_ids, union_size,
+                    stream);
+    if (st != MOE_OK || d.T == 0) return st;
+    return moe_expert_ffn(x, w13, w2, offsets, perm_token, union_ids, union_size, d, y_perm, ws,
+                          ws_bytes, stream);
+  }
+  if (!x || !w13 || !w2 || !y_perm || !ws) return MOE_ERR_INVALID;
+  st = check_routed(d, topk_ids, counts, offsets, perm_token, pair_pos, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(y_perm) || !aligned128(ws))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), w13, offsets, perm_token, union_ids + d.E,
+                   union_size, ws, d.I, d.H, 0, d.E, nullptr, nullptr,
+                   topk_ids, d.T, d.K, counts, offsets, perm_token, pair_pos, union_ids,
+                   union_size};
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kBf16>(d);
+  eldr::FfnArgs dn{reinterpret_cast<const uint4*>(ws), w2, offsets, perm_token, union_ids + d.E,
+                   union_size, y_perm, d.H, d.I, 0, d.E, nullptr, nullptr};
+  dn.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kBf16>(d);
+  eldr::launch_ffn_fused<eldr::kBf16>(up, dn, sync, d.T, d.E, reinterpret_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" int moe_expert_ffn_mxfp4_routed(const float* x, const uint8_t* up_codes,
+                                           const uint8_t* up_scales, const uint8_t* down_codes,
+                                           const uint8_t* down_scales, const int32_t* topk_ids,
+                                           moe_dims d, int32_t* counts, int32_t* offsets,
+                                           int32_t* perm_token, int32_t* pair_pos,
+                                           int32_t* union_ids, int32_t* union_size, float* y_perm,
+                                           void* ws, size_t ws_bytes, int32_t* sync,
+                                           void* stream) {
+  using namespace eldr_host;
+  int st = check_mxfp4_dims(d);
+  if (st != MOE_OK) return st;
+  if (!sync) return MOE_ERR_INVALID;
+  if (!aligned4(sync)) return MOE_ERR_UNSUPPORTED;
+  if (d.T == 0 || d.T > 64) {
+    st = moe_bucket(topk_ids, d, counts, offsets, perm_token, pair_pos, union_ids, union_size,
+                    stream);
+    if (st != MOE_OK || d.T == 0) return st;
+    return moe_expert_ffn_mxfp4(x, up_codes, up_scales, down_codes, down_scales, offsets,
+                                perm_token, union_ids, union_size, d, y_perm, ws, ws_bytes, stream);
+  }
+  if (!x || !up_codes || !up_scales || !down_codes || !down_scales || !y_perm || !ws)
+    return MOE_ERR_INVALID;
+  st = check_routed(d, topk_ids, counts, offsets, perm_token, pair_pos, union_ids, union_size);
+  if (st != MOE_OK) return st;
+  if (!aligned16(x) || !aligned16(up_codes) || !aligned4(up_scales) || !aligned16(down_codes) ||
+      !aligned4(down_scales) || !aligned16(y_perm) || !aligned128(ws))
+    return MOE_ERR_UNSUPPORTED;
+  if (ws_bytes < moe_ffn_workspace_bytes(d)) return MOE_ERR_WORKSPACE;
+  eldr::FfnArgs up{reinterpret_cast<const uint4*>(x), nullptr, offsets, perm_token,
+                   union_ids + d.E, union_size, ws, d.I, d.H, 0, d.E,
+                   reinterpret_cast<const eldr::u32x4*>(up_codes),
+                   reinterpret_cast<const uint32_t*>(up_scales),
+                   topk_ids, d.T, d.K, counts, offsets, perm_token, pair_pos, union_ids,
+                   union_size};
+  up.tiles = eldr::ffn_tiles<eldr::kUp, eldr::kMxfp4>(d);
+  eldr::FfnArgs dn{reinterpret_cast<const uint4*>(ws), nullptr, offsets, perm_token,
+                   union_ids + d.E, union_size, y_perm, d.H, d.I, 0, d.E,
+                   reinterpret_cast<const eldr::u32x4*>(down_codes),
+                   reinterpret_cast<const uint32_t*>(down_scales)};
+  dn.tiles = eldr::ffn_tiles<eldr::kDown, eldr::kMxfp4>(d);
+  eldr::launch_ffn_fused<eldr::kMxfp4>(up, dn, sync, d.T, d.E,
+                                       reinterpret_cast<hipStream_t>(stream));
   return launch_status();
 }

@@ -59,14 +59,14 @@ class Layer:
             out.append(h)
         return tuple(out)
 
-    def run(self, routing=None, fused: bool = True):
-        """Run the layer (buckets fused into the up projection, or a separate
-        moe_bucket call); return host copies of every output."""
+    def run(self, routing=None, path: str = "routed"):
+        """Run the layer (the expert FFN by one of binding.FFN_PATHS); return
+        host copies of every output."""
         if routing is not None:
             routing = (torch.from_numpy(np.ascontiguousarray(routing[0], np.int32)).cuda(),
                        torch.from_numpy(np.ascontiguousarray(routing[1], np.float32)).cuda())
         B.moe_layer(self.x, self.wg, self.p13, self.p2, self.d, self.buf, routing=routing,
-                    fused=fused)
+                    path=path)
         torch.cuda.synchronize()
         return fetch(self.buf, self.d)
 

@@ -228,6 +228,37 @@ def test_routed_up_validates_on_host(lib):
     assert fns[1](B.dims(64, 2048 + 32, 128, 8, 768)) == B.MOE_ERR_UNSUPPORTED
 
 
+def test_fused_ffn_validates_on_host(lib):
+    # moe_expert_ffn_routed / _mxfp4: the sync buffer's null and alignment
+    # checks, then those of moe_bucket and moe_expert_ffn, before any launch.
+    def bf16(d, ids=FAKE, cnt=FAKE, ws_bytes=1 << 40, x=FAKE, y=FAKE, sync=FAKE, ws=FAKE):
+        return lib.moe_expert_ffn_routed(x, FAKE, FAKE, ids, d, cnt, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                         y, ws, ws_bytes, sync, None)
+
+    def mx(d, ids=FAKE, cnt=FAKE, ws_bytes=1 << 40, x=FAKE, y=FAKE, sync=FAKE, ws=FAKE):
+        return lib.moe_expert_ffn_mxfp4_routed(x, FAKE, FAKE, FAKE, FAKE, ids, d, cnt, FAKE, FAKE,
+                                               FAKE, FAKE, FAKE, y, ws, ws_bytes, sync, None)
+
+    for f in (bf16, mx):
+        assert f(B.dims(64, 2048, 128, 129, 768)) == B.MOE_ERR_INVALID         # K > E
+        assert f(B.dims(64, 2048, 257, 8, 768)) == B.MOE_ERR_UNSUPPORTED       # E above the limit
+        assert f(B.dims(*GOOD), sync=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), sync=ctypes.c_void_p(0x10002)) == B.MOE_ERR_UNSUPPORTED
+        assert f(B.dims(*GOOD), ids=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), cnt=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), x=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), y=None) == B.MOE_ERR_INVALID
+        assert f(B.dims(*GOOD), ids=ctypes.c_void_p(0x10002)) == B.MOE_ERR_UNSUPPORTED
+        assert f(B.dims(*GOOD), y=FAKE_MIS) == B.MOE_ERR_UNSUPPORTED
+        # h rows must be whole 128-byte lines for the in-launch hand-over
+        assert f(B.dims(*GOOD), ws=ctypes.c_void_p(0x10010)) == B.MOE_ERR_UNSUPPORTED
+        d = B.dims(*GOOD)
+        assert f(d, ws_bytes=B.moe_ffn_workspace_bytes(d) - 1) == B.MOE_ERR_WORKSPACE
+    assert mx(B.dims(64, 2048 + 32, 128, 8, 768)) == B.MOE_ERR_UNSUPPORTED
+    assert lib.moe_ffn_sync_bytes(B.dims(*GOOD)) == 4 * (2 * 128 + 1)
+    assert lib.moe_ffn_sync_bytes(B.dims(64, 2048, 128, 129, 768)) == 0
+
+
 def test_noalloc_ffn_rejects_oversize_on_host(lib):
     # The fixed workspace holds 32 MiB; a larger problem is refused before the
     # library touches a device.

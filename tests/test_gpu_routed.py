@@ -1,14 +1,19 @@
-"""The routed up launch (buckets built inside the up projection) against the
-separate calls, bit for bit.
+"""The routed launches (buckets built inside the FFN) against the separate
+calls, bit for bit.
 
-moe_expert_ffn_up_routed must leave exactly what moe_bucket followed by
-moe_expert_ffn_up leaves: every bucket output (counts, offsets, perm_token,
-pair_pos, both halves of union_ids, union_size) and the workspace h, and so
-the same y and layer output; the separate calls are themselves checked
-against the oracle in the parity tests, and moe_layer (which takes the routed
-launch) is checked against the oracle there too.  The third path,
-moe_bucket then moe_expert_ffn (up and down in one call), must agree as well.
+moe_expert_ffn_routed (buckets, up and down projections in one launch) and
+moe_expert_ffn_up_routed (buckets and up projection) must leave exactly what
+moe_bucket followed by moe_expert_ffn_up and moe_expert_ffn_down leaves: every
+bucket output (counts, offsets, perm_token, pair_pos, both halves of
+union_ids, union_size), the workspace h, y and the layer output; the separate
+calls are themselves checked against the oracle in the parity tests, and
+moe_layer (whose default is the routed up launch) is checked against the
+oracle there too.  A fourth path, moe_bucket then moe_expert_ffn (up and down in one
+call), must agree as well.  The one-launch path's sync counters must be zero
+after every call, and its wait must never have given up.
 """
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -43,16 +48,25 @@ def _poison(buf):
     buf.out.fill_(float("nan"))
 
 
-def _three_paths(layer: G.Layer, routing):
-    """The layer by the routed launch, by moe_bucket + moe_expert_ffn_up/down, and
-    by moe_bucket + moe_expert_ffn; returns the three snapshots."""
+PATHS = ("fused", "routed", "split", "combined")
+
+
+def _check_sync(buf):
+    sync = buf.sync.cpu().numpy()
+    assert sync[-1] == 0, "a down band of the one-launch FFN gave up waiting for h"
+    assert not sync.any(), "the one-launch FFN left its counters non-zero"
+
+
+def _all_paths(layer: G.Layer, routing):
+    """The layer by each FFN path of moe_layer, and by moe_bucket +
+    moe_expert_ffn; returns the snapshots in PATHS order."""
     d, buf = layer.d, layer.buf
     r = None
     if routing is not None:
         r = (torch.from_numpy(np.ascontiguousarray(routing[0], np.int32)).cuda(),
              torch.from_numpy(np.ascontiguousarray(routing[1], np.float32)).cuda())
     snaps = []
-    for path in ("routed", "separate", "combined"):
+    for path in PATHS:
         _poison(buf)
         if path == "combined":
             ids, w = B._gate(layer.x, layer.wg, d, buf, r, None)
@@ -62,10 +76,10 @@ def _three_paths(layer: G.Layer, routing):
                              buf.union_ids, buf.union_size, d, buf.y_perm, buf.ws)
             B.moe_combine(buf.y_perm, buf.pair_pos, w, d, buf.out)
         else:
-            B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r,
-                        fused=path == "routed")
+            B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r, path=path)
         torch.cuda.synchronize()
         snaps.append(_snapshot(buf, d))
+        _check_sync(buf)
     return snaps
 
 
@@ -82,7 +96,7 @@ def _assert_equal(snaps, valid=True):
 def test_routed_equals_separate_gate_routed(T):
     G.say(f"case: routed vs separate calls, qwen shape T={T}, gate-routed")
     layer = G.Layer(QWEN, T, seed=60 + T, experts_on_host=False)
-    snaps = _three_paths(layer, None)
+    snaps = _all_paths(layer, None)
     _assert_equal(snaps)
     G.say(f"  union {int(snaps[0]['union_size'][0])}")
 
@@ -92,7 +106,7 @@ def test_routed_equals_separate_controlled(U):
     G.say(f"case: routed vs separate calls, qwen shape T=64, controlled union U={U}")
     layer = G.Layer(QWEN, 64, seed=70, experts_on_host=False)
     ids, w, _ = synth.controlled_routing(64, QWEN.E, QWEN.K, U, seed=U)
-    _assert_equal(_three_paths(layer, (ids, w)))
+    _assert_equal(_all_paths(layer, (ids, w)))
 
 
 @pytest.mark.parametrize("name,E,K,H,I,T", [
@@ -105,16 +119,16 @@ def test_routed_equals_separate_controlled(U):
 def test_routed_equals_separate_shapes(name, E, K, H, I, T):
     G.say(f"case: routed vs separate calls, {name} E={E} top-{K} H={H} I={I} T={T}")
     layer = G.Layer(synth.LayerShape(name, E=E, K=K, H=H, I=I), T, seed=E + T, experts_on_host=False)
-    _assert_equal(_three_paths(layer, None))
+    _assert_equal(_all_paths(layer, None))
 
 
-def test_routed_large_batch_takes_two_launches():
-    # Above 64 tokens the routed entry point runs moe_bucket and the up launch.
+def test_routed_large_batch_takes_separate_launches():
+    # Above 64 tokens the routed entry points run moe_bucket and the FFN launches.
     G.say("case: routed vs separate calls, qwen shape T=65 and T=128, controlled U=32")
     for T in (65, 128):
         layer = G.Layer(QWEN, T, seed=80, experts_on_host=False)
         ids, w, _ = synth.controlled_routing(T, QWEN.E, QWEN.K, 32, seed=T)
-        _assert_equal(_three_paths(layer, (ids, w)))
+        _assert_equal(_all_paths(layer, (ids, w)))
 
 
 def test_routed_invalid_routing():
@@ -124,7 +138,7 @@ def test_routed_invalid_routing():
     for ids in (np.array([[1, 1], [2, 3], [4, 5], [6, 7]], np.int32),
                 np.array([[1, 16], [2, 3], [4, 5], [6, 7]], np.int32),
                 np.array([[-1, 2], [2, 3], [4, 5], [6, 7]], np.int32)):
-        snaps = _three_paths(layer, (ids, w))
+        snaps = _all_paths(layer, (ids, w))
         assert int(snaps[0]["union_size"][0]) == -1
         _assert_equal(snaps, valid=False)
         assert np.isnan(snaps[0]["y_perm"]).all(), "the FFN wrote outputs for invalid routing"
@@ -147,7 +161,7 @@ def test_routed_empty_batch():
     assert bool((buf.union_ids == -1).all())
 
 
-@pytest.mark.parametrize("T", [8, 24, 64])
+@pytest.mark.parametrize("T", [8, 24, 64, 65])
 def test_routed_mxfp4_equals_separate(T):
     G.say(f"case: MXFP4 routed vs separate calls, E=16 top-4 H=640 I=320 T={T}, gate-routed")
     sh = synth.LayerShape("mx_routed", E=16, K=4, H=640, I=320)
@@ -158,9 +172,55 @@ def test_routed_mxfp4_equals_separate(T):
     d = B.dims(T, sh.H, sh.E, sh.K, sh.I)
     buf = B.LayerBuffers.allocate(d)
     snaps = []
-    for fused in (True, False):
+    for path in B.FFN_PATHS:
         _poison(buf)
-        B.moe_layer_mxfp4(x, wg, up, down, d, buf, fused=fused)
+        B.moe_layer_mxfp4(x, wg, up, down, d, buf, path=path)
         torch.cuda.synchronize()
         snaps.append(_snapshot(buf, d))
+        _check_sync(buf)
     _assert_equal(snaps)
+
+
+def test_fused_back_to_back_calls():
+    # Twelve one-launch layers queued without a host synchronisation between
+    # them, over changing routings and union sizes on one sync buffer: each
+    # launch finds the counters its predecessor reset, and each result equals
+    # the separate calls' on the same routing.
+    G.say("case: one-launch FFN, 12 back-to-back calls on one sync buffer, qwen shape T=64")
+    layer = G.Layer(QWEN, 64, seed=91, experts_on_host=False)
+    d, buf = layer.d, layer.buf
+    routings = []
+    for i, U in enumerate((16, 128, 32, 64, 8, 127, 96, 24, 40, 128, 16, 72)):
+        ids, w, _ = synth.controlled_routing(64, QWEN.E, QWEN.K, U, seed=100 + i)
+        routings.append((torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda()))
+    outs = []
+    for r in routings:
+        B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r)
+        outs.append((buf.y_perm[:d.T * d.K].clone(), buf.out.clone()))
+    torch.cuda.synchronize()
+    _check_sync(buf)
+    for i, r in enumerate(routings):
+        B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r, path="split")
+        torch.cuda.synchronize()
+        assert torch.equal(outs[i][0], buf.y_perm[:d.T * d.K]), f"y_perm of call {i}"
+        assert torch.equal(outs[i][1], buf.out), f"out of call {i}"
+
+
+def test_fused_entry_point_checks():
+    # A null or misaligned sync buffer is refused before any launch; T = 0
+    # and T > 64 leave the buffer untouched.
+    G.say("case: one-launch FFN argument checks, tiny shape")
+    layer = G.Layer(TINY, 4, seed=5, experts_on_host=False)
+    d, buf = layer.d, layer.buf
+    ids, w = B._gate(layer.x, layer.wg, d, buf, None, None)
+    lib = B.load()
+    args = [B._ptr(layer.x), B._ptr(layer.p13), B._ptr(layer.p2), B._ptr(ids), d,
+            B._ptr(buf.counts), B._ptr(buf.offsets), B._ptr(buf.perm_token), B._ptr(buf.pair_pos),
+            B._ptr(buf.union_ids), B._ptr(buf.union_size), B._ptr(buf.y_perm), B._ptr(buf.ws),
+            buf.ws.numel() * 4]
+    assert lib.moe_expert_ffn_routed(*args, None, None) == B.MOE_ERR_INVALID
+    spare = torch.zeros(2 * d.E + 2, dtype=torch.int32, device="cuda")
+    misaligned = ctypes.c_void_p(spare.data_ptr() + 2)
+    assert lib.moe_expert_ffn_routed(*args, misaligned, None) == B.MOE_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert not spare.any()
