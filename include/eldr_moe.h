@@ -277,9 +277,10 @@ int moe_expert_ffn_up_routed(const float* x, const uint16_t* w13, const int32_t*
  * y_perm, ws, ws_bytes as for moe_expert_ffn, whose y_perm (and workspace)
  * results it leaves, bit for bit; ws must be 128-byte aligned here (else
  * MOE_ERR_UNSUPPORTED).
- * sync: int32 [2E + 1] (moe_ffn_sync_bytes), caller-owned device memory that
- * must be zero before the first call; every call leaves it zero.  Entries
- * 0 .. 2E-1 are per-expert counters of the call; entry 2E becomes 1 if a
+ * sync: int32 [64 E + 1] (moe_ffn_sync_bytes), caller-owned device memory
+ * that must be zero before the first call; every call leaves it zero.  Words
+ * 0 .. 64E-1 hold two counters per union position, one 256-byte line each (so
+ * that the waits' polls spread over memory channels); word 64E becomes 1 if a
  * down band gave up waiting for its expert (a bounded wait of about 2^18
  * polls that a correct run never reaches: the GPU starts an XCD's
  * workgroups in index order and every up band precedes every down band of
@@ -295,7 +296,7 @@ int moe_expert_ffn_routed(const float* x, const uint16_t* w13, const uint16_t* w
                           int32_t* perm_token, int32_t* pair_pos, int32_t* union_ids,
                           int32_t* union_size, float* y_perm, void* ws, size_t ws_bytes,
                           int32_t* sync, void* stream);
-/* Bytes of moe_expert_ffn_routed's sync buffer: 4 (2E + 1); 0 for invalid dims. */
+/* Bytes of moe_expert_ffn_routed's sync buffer: 4 (64 E + 1); 0 for invalid dims. */
 size_t moe_ffn_sync_bytes(moe_dims d);
 
 /*

@@ -267,7 +267,8 @@ def _need_sync(sync, d: MoeDims) -> None:
 def moe_expert_ffn_routed(x, w13, w2, topk_ids, d: MoeDims, counts, offsets, perm_token, pair_pos,
                           union_ids, union_size, y_perm, ws, sync, stream=None) -> None:
     """moe_bucket then moe_expert_ffn, one launch for T <= 64.  ``sync`` is an
-    int32 [2E + 1] device tensor, zero before the first call (left zero)."""
+    int32 [64 E + 1] device tensor (moe_ffn_sync_bytes), zero before the first
+    call (left zero)."""
     _need(x, "x", torch.float32, d.T * d.H)
     _need(w13, "w13", torch.bfloat16, 2 * d.E * d.I * d.H)
     _need(w2, "w2", torch.bfloat16, d.E * d.H * d.I)

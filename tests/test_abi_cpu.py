@@ -255,7 +255,7 @@ def test_fused_ffn_validates_on_host(lib):
         d = B.dims(*GOOD)
         assert f(d, ws_bytes=B.moe_ffn_workspace_bytes(d) - 1) == B.MOE_ERR_WORKSPACE
     assert mx(B.dims(64, 2048 + 32, 128, 8, 768)) == B.MOE_ERR_UNSUPPORTED
-    assert lib.moe_ffn_sync_bytes(B.dims(*GOOD)) == 4 * (2 * 128 + 1)
+    assert lib.moe_ffn_sync_bytes(B.dims(*GOOD)) == 4 * (64 * 128 + 1)
     assert lib.moe_ffn_sync_bytes(B.dims(64, 2048, 128, 129, 768)) == 0
 
 
