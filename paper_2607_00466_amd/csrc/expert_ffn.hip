@@ -38,11 +38,12 @@
 //   more 16-token tiles first, equal ones by ascending id.  With at most 64
 //   tokens an expert, the union's experts go round-robin, all of an
 //   expert's bands on one XCD (sharing its L2 for the expert's
-//   activations).  With more, bucket sizes are skewed, and the union's
-//   (expert, band) units go round-robin instead, so every XCD gets an equal
-//   share of every expert; a band's token groups stay on one XCD, next to
-//   each other, so their shared weight reads meet in its L2.  Either way an
-//   XCD runs its largest buckets first.
+//   activations).  With more, whole experts are still dealt while every
+//   bucket fits one token group; once one does not, bucket sizes are skewed,
+//   and the union's (expert, band) units go round-robin instead, so every XCD
+//   gets an equal share of every expert; a band's token groups stay on one
+//   XCD, next to each other, so their shared weight reads meet in its L2.
+//   Either way an XCD runs its largest buckets first.
 // * Weights come in one of two formats (a template parameter): bf16, or
 //   MXFP4 (FP4 E2M1 codes with one E8M0 scale per 32 values along the
 //   reduction axis, the format the paper serves GPT-OSS-120B in), whose
@@ -861,8 +862,9 @@ void ffn_kernel(FfnArgs a) {
   // different tokens run side by side and share the XCD's L2.  A slot takes
   // items slot, slot + slots, ... .  Without MULTI (batches of at most
   // kGroupTokens tokens) every expert has one group and the expert at union
-  // position u belongs to XCD u % 8; with it, the union's (expert, band)
-  // units are dealt round-robin.
+  // position u belongs to XCD u % 8; with it, the same holds while every
+  // bucket fits one group, and otherwise the union's (expert, band) units are
+  // dealt round-robin.
   const int tid = threadIdx.x;
   const int lane = tid % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -937,6 +939,32 @@ void ffn_kernel(FfnArgs a) {
       n_j[j] = nb * g;
       first_j[j] = lane_n;
       lane_n += n_j[j];
+    }
+    // When every bucket fits one token group, the batch is not skewed enough
+    // to need the band dealing: whole experts go round-robin over the XCDs as
+    // for small batches, so that an expert's activations (x rows for up, h
+    // for down) are fetched into one XCD's L2 rather than into all eight.
+    int cmax = max(max(c_j[0], c_j[1]), max(c_j[2], c_j[3]));
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) cmax = max(cmax, __shfl_xor(cmax, off));
+    if (__builtin_amdgcn_readfirstlane(cmax) <= kGroupTokens) {
+      const int u = (slot / a.tiles) * kNumXcd + xcd;
+      if (u >= U || u >= a.experts) return;  // also covers U < 0 (invalid routing)
+      // union position u: its entries, from the lane that holds them
+      const int ls = u / 4, js = u % 4;
+      int ie = 0, isb = 0, ic = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (j == js) {
+          ie = __builtin_amdgcn_readlane(e_j[j], ls);
+          isb = __builtin_amdgcn_readlane(sb_j[j], ls);
+          ic = __builtin_amdgcn_readlane(c_j[j], ls);
+        }
+      }
+      if (ic > 0)
+        ffn_item<MODE, NT, FMT, MODE == kDown, false, false, false>(a, L, ie, slot % a.tiles, isb, 0, ic,
+                                                                   NoHook{}, NoHook{});
+      return;
     }
     const int incl = wave_inclusive_sum(lane_n);
     const int total = __builtin_amdgcn_readlane(incl, kWave - 1);

@@ -131,8 +131,9 @@ def test_heavy_experts_on_one_xcd():
 @pytest.mark.parametrize("T", [64, 100])
 def test_most_experts(T):
     # E = 256, the most the library takes: the union reaches the last of the
-    # four union positions a lane holds in the FFN's lookup.  T = 64 deals
-    # whole experts over the XCDs, T = 100 deals (expert, band) units.
+    # four union positions a lane holds in the FFN's lookup.  T = 64 takes the
+    # small-batch kernels, T = 100 the large-batch ones (whose buckets all fit
+    # one 128-token group here, so they too deal whole experts).
     G.say(f"case: E=256 top-8 H=256 I=128 T={T}, gate-routed")
     shape = synth.LayerShape("most_experts", E=256, K=8, H=256, I=128)
     layer = G.Layer(shape, T, seed=30 + T)
@@ -160,6 +161,20 @@ def test_most_experts_heavy_buckets():
     assert g["union_size"] > 192
     assert g["counts"][heavy].tolist() == [T] * 4
     assert g["union_ids"][256:260].tolist() == heavy.tolist()  # first in dispatch order
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+@pytest.mark.parametrize("n", [128, 129])
+def test_large_batch_dealing_boundary(n):
+    # Batches over 64 tokens deal whole experts over the XCDs while every
+    # bucket fits one 128-token group, and (expert, band) units once one does
+    # not: a bucket of 128 tokens takes the first, 129 the second.
+    G.say(f"case: qwen layer T=160, expert 3 takes {n} tokens, the others light")
+    T = 160
+    ids, w = G.fixed_bucket_routing(T, QWEN.E, QWEN.K, [(3, n)], seed=n)
+    layer = G.Layer(QWEN, T, seed=15)
+    g = layer.run(routing=(ids, w))
+    assert int(g["counts"][3]) == n and int(g["counts"].max()) == n
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
@@ -192,7 +207,7 @@ def test_k_equals_e():
 @pytest.mark.parametrize("T", [5, 70])
 def test_single_expert(T):
     # E = K = 1: every token on expert 0 with weight 1, a union of one.  T = 70
-    # gives that expert two token groups (the (expert, band) dealing).
+    # takes the large-batch kernels with one 128-token group.
     G.say(f"case: E=1 top-1 H=256 I=128 T={T}, gate-routed")
     shape = synth.LayerShape("single_expert", E=1, K=1, H=256, I=128)
     layer = G.Layer(shape, T, seed=40 + T)
