@@ -710,7 +710,7 @@ __device__ __forceinline__ bool route_buckets(const FfnArgs& a, RouteLds& R, Pic
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave;
-  const int T = a.T, K = a.K, E = a.experts, P = a.T * a.K;
+  const int K = a.K, E = a.experts, P = a.T * a.K;
   constexpr int kIdsPerThread = 64 * MOE_MAX_K / kThreads;
   int idv[kIdsPerThread];
 #pragma unroll
