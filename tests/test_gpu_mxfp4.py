@@ -210,6 +210,20 @@ def test_mxfp4_big_buckets_take_token_groups():
     _check_layer(layer, g, (ids, w))
 
 
+@pytest.mark.parametrize("n", [64, 65])
+def test_mxfp4_large_batch_dealing_boundary(n):
+    # Batches over 64 tokens deal whole experts while every bucket fits one
+    # 64-token MXFP4 group, and (expert, band) units once one does not.
+    sh = synth.LayerShape("mx_dealing", E=16, K=4, H=256, I=192)
+    T = 80
+    G.say(f"case: MXFP4 E=16 top-4 H=256 I=192 T={T}, expert 5 takes {n} tokens")
+    ids, w = G.fixed_bucket_routing(T, sh.E, sh.K, [(5, n)], seed=n)
+    layer = MxLayer(sh, T, seed=n)
+    g = layer.run((ids, w))
+    assert int(g["counts"][5]) == n and int(g["counts"].max()) == n
+    _check_layer(layer, g, routing=(ids, w))
+
+
 def test_mxfp4_empty_batch_and_invalid_routing():
     G.say("case: MXFP4 empty batch, then a duplicated id (invalid routing)")
     sh = synth.LayerShape("mx_edge", E=8, K=2, H=128, I=64)

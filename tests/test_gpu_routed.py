@@ -224,3 +224,51 @@ def test_fused_entry_point_checks():
     assert lib.moe_expert_ffn_routed(*args, misaligned, None) == B.MOE_ERR_UNSUPPORTED
     torch.cuda.synchronize()
     assert not spare.any()
+
+
+def test_fused_graph_replays():
+    # The one-launch FFN captured in a HIP graph: its sync counters carry over
+    # from replay to replay, so every replay (with eager work between) must
+    # equal the eager result, leave the counters zero, and follow new routing
+    # written in place.
+    G.say("case: one-launch FFN in a HIP graph, qwen shape T=64, controlled U=32 then U=96")
+    layer = G.Layer(QWEN, 64, seed=240, experts_on_host=False)
+    d, buf = layer.d, layer.buf
+    ids, w, _ = synth.controlled_routing(64, QWEN.E, QWEN.K, 32, seed=7)
+    r = (torch.from_numpy(ids).cuda(), torch.from_numpy(w).cuda())
+    run = lambda: B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r,  # noqa: E731
+                              path="fused")
+    run()
+    torch.cuda.synchronize()
+    eager = buf.out.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        buf.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf.out, eager), f"replay {rep}"
+        _check_sync(buf)
+        scratch = torch.randn(2048, device="cuda").sum()  # unrelated eager work between replays
+        torch.cuda.synchronize()
+        del scratch
+    ids2, w2, _ = synth.controlled_routing(64, QWEN.E, QWEN.K, 96, seed=8)
+    r[0].copy_(torch.from_numpy(ids2))
+    r[1].copy_(torch.from_numpy(w2))
+    B.moe_layer(layer.x, layer.wg, layer.p13, layer.p2, d, buf, routing=r, path="split")
+    torch.cuda.synchronize()
+    eager2 = buf.out.clone()
+    buf.out.zero_()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(buf.out, eager2)
+    assert not torch.equal(eager, eager2)
+    _check_sync(buf)
