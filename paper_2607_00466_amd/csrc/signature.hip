@@ -9,9 +9,11 @@
 // into the neighbouring cell; integer atomics make the result independent of
 // the order of the picks.
 //
-// request counts: one thread per 4-cell word of a request's [L, E] row,
-// summing that word over the request's blocks (coalesced 32-bit loads of
-// consecutive words of each block's row) into four int32 counts.
+// request counts: a workgroup per (request, 1 KB stretch of the [L, E] row).
+// Its four waves split the request's blocks, 16 at a time a wave; a lane
+// reads 16 cells of each block (one 16-byte load), all 16 blocks' loads in
+// flight before the first is used, and keeps 16 int32 sums.  The four waves'
+// sums then meet in LDS, and each thread writes four of the stretch's counts.
 #include "common.hpp"
 #include "eldr_signature.h"
 
@@ -56,31 +58,87 @@ __global__ __launch_bounds__(kSigThreads) void sig_reset_kernel(const int32_t* _
   if (w < row_words) sig_words[(int64_t)b * row_words + w] = 0u;
 }
 
-__global__ __launch_bounds__(kSigThreads) void sig_request_kernel(
+constexpr int kReqWaves = 4;
+constexpr int kReqWords = 4 * kWave;  // row words a workgroup covers: 4 a lane (1 KB)
+constexpr int kReqUnroll = 16;        // blocks a wave has in flight
+
+// VEC: every row starts 16-byte aligned and holds a whole number of 16-byte
+// pieces (row_words % 4 == 0), so a lane reads its 4 words with one load;
+// otherwise word by word, each within the row.
+template <bool VEC>
+__global__ __launch_bounds__(kReqWaves * kWave) void sig_request_kernel(
     const uint32_t* __restrict__ sig_words, const int32_t* __restrict__ block_table,
     const int32_t* __restrict__ n_blocks, int max_blocks, int row_words, int num_blocks,
     int4* __restrict__ out) {
+  __shared__ int4 part[kReqWaves][kWave][4];
   const int r = blockIdx.y;
-  const int w = blockIdx.x * kSigThreads + threadIdx.x;
-  if (w >= row_words) return;
-  // An empty cache (num_blocks == 0, sig may be null) contributes nothing.
-  const int n = num_blocks > 0 ? min(max(n_blocks[r], 0), max_blocks) : 0;
-  const int32_t* table = block_table + (int64_t)r * max_blocks;
-  // Branch-free and unrolled, so a thread has several block loads in flight:
-  // an invalid block id reads block 0's word and adds nothing.
-  int4 acc = make_int4(0, 0, 0, 0);
-#pragma unroll 8
-  for (int i = 0; i < n; ++i) {
-    const int b = table[i];
-    const bool ok = b >= 0 && b < num_blocks;
-    const uint32_t v = sig_words[(int64_t)(ok ? b : 0) * row_words + w] & (ok ? 0xffffffffu : 0u);
-    // the four int8 cells of the word, sign-extended (cell 0 is the low byte)
-    acc.x += (int)(int8_t)(v & 0xffu);
-    acc.y += (int)(int8_t)((v >> 8) & 0xffu);
-    acc.z += (int)(int8_t)((v >> 16) & 0xffu);
-    acc.w += (int)(int8_t)(v >> 24);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const int w0 = blockIdx.x * kReqWords + 4 * lane;  // the lane's first word
+  int acc[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) acc[c] = 0;
+  // Group g holds blocks [g * 64, g * 64 + 64); wave w takes 16 consecutive
+  // ones.  The first group is issued before n is known: its table entries
+  // are read up to max_blocks (in the table), so that the table and n arrive
+  // together.  Entries past n, and invalid block ids, read block 0's words
+  // and add nothing.  An empty cache (num_blocks == 0, sig may be null)
+  // contributes nothing and is not read.
+  if (num_blocks > 0) {
+    const int n = min(max(n_blocks[r], 0), max_blocks);
+    const int32_t* table = block_table + (int64_t)r * max_blocks;
+    int i0 = wave * kReqUnroll;
+    do {
+      u32x4 v[kReqUnroll];
+#pragma unroll
+      for (int k = 0; k < kReqUnroll; ++k) {
+        const int i = i0 + k;
+        const int b = i < max_blocks ? table[i] : -1;
+        const bool ok = i < n && b >= 0 && b < num_blocks;
+        const uint32_t* row = sig_words + (int64_t)(ok ? b : 0) * row_words;
+        const uint32_t m = ok ? 0xffffffffu : 0u;
+        if constexpr (VEC) {
+          const u32x4 x = w0 < row_words ? *reinterpret_cast<const u32x4*>(row + w0) : u32x4{0u, 0u, 0u, 0u};
+          v[k] = x & m;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[k][q] = (w0 + q < row_words ? row[w0 + q] : 0u) & m;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kReqUnroll; ++k) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // the four int8 cells of the word, sign-extended (cell 0 is the low byte)
+          const uint32_t x = v[k][q];
+          acc[4 * q + 0] += (int)(int8_t)(x & 0xffu);
+          acc[4 * q + 1] += (int)(int8_t)((x >> 8) & 0xffu);
+          acc[4 * q + 2] += (int)(int8_t)((x >> 16) & 0xffu);
+          acc[4 * q + 3] += (int)(int8_t)(x >> 24);
+        }
+      }
+      i0 += kReqWaves * kReqUnroll;
+    } while (i0 < n);
   }
-  out[(int64_t)r * row_words + w] = acc;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    part[wave][lane][q] = make_int4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+  __syncthreads();
+  // thread t: word 4 * (t / 4) + t % 4 of the stretch, i.e. word blockIdx.x * kReqWords + t
+  const int t = threadIdx.x;
+  const int w = blockIdx.x * kReqWords + t;
+  if (w < row_words) {
+    int4 sum = make_int4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < kReqWaves; ++j) {
+      const int4 p = part[j][t / 4][t % 4];
+      sum.x += p.x;
+      sum.y += p.y;
+      sum.z += p.z;
+      sum.w += p.w;
+    }
+    out[(int64_t)r * row_words + w] = sum;
+  }
 }
 
 }  // namespace eldr
@@ -152,10 +210,16 @@ extern "C" int moe_sig_request_counts(const int8_t* sig, const int32_t* block_ta
       (sig && !aligned4(sig)))
     return MOE_ERR_UNSUPPORTED;
   const int row_words = L * E / 4;
-  dim3 grid((row_words + eldr::kSigThreads - 1) / eldr::kSigThreads, R);
-  hipLaunchKernelGGL(eldr::sig_request_kernel, grid, dim3(eldr::kSigThreads), 0,
-                     reinterpret_cast<hipStream_t>(stream),
-                     reinterpret_cast<const uint32_t*>(sig), block_table, n_blocks, max_blocks,
-                     row_words, num_blocks, reinterpret_cast<int4*>(out));
+  const dim3 grid((row_words + eldr::kReqWords - 1) / eldr::kReqWords, R);
+  const dim3 block(eldr::kReqWaves * eldr::kWave);
+  const bool vec = row_words % 4 == 0 && (!sig || aligned16(sig));
+  if (vec)
+    hipLaunchKernelGGL(eldr::sig_request_kernel<true>, grid, block, 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const uint32_t*>(sig), block_table, n_blocks, max_blocks, row_words,
+                       num_blocks, reinterpret_cast<int4*>(out));
+  else
+    hipLaunchKernelGGL(eldr::sig_request_kernel<false>, grid, block, 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const uint32_t*>(sig), block_table, n_blocks, max_blocks, row_words,
+                       num_blocks, reinterpret_cast<int4*>(out));
   return launch_status();
 }

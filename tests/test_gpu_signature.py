@@ -176,6 +176,35 @@ def test_request_counts_many_requests_ragged_tables():
         assert np.array_equal(got[r], SO.request_counts(c.ref, valid)), r
 
 
+@pytest.mark.parametrize("L,E,offset", [(3, 20, 0), (9, 128, 4), (6, 64, 0)])
+def test_request_counts_load_paths(L, E, offset):
+    # Rows of 15 words (not whole 16-byte pieces) and a cache 4 bytes off
+    # 16-byte alignment take the word-by-word reads; tables of up to 150
+    # blocks take several groups of 64 with a ragged last one.
+    G.say(f"case: request counts, L={L} E={E}, cache offset {offset} bytes, tables of 0..150 blocks")
+    nb, T = 40, 500
+    rng = np.random.default_rng(20 + L)
+    ids = synth.prefill_picks(L, T, E, 8, seed=21 + L)
+    tb = rng.integers(0, nb, T).astype(np.int32)
+    ref, _ = SO.capture(SO.new_cache(nb, L, E), ids, tb)
+    flat = torch.zeros(nb * L * E + 16, dtype=torch.int8, device="cuda")
+    sig = flat[offset:offset + nb * L * E].view(nb, L, E)
+    B.moe_sig_capture(dev(ids), dev(tb), 0, L, E, sig)
+    torch.cuda.synchronize()
+    assert np.array_equal(sig.cpu().numpy().astype(np.int64), ref)
+    sizes = (150, 64, 65, 1, 0, 129, 17)
+    tables = [list(rng.integers(-2, nb + 2, n)) for n in sizes]
+    table = np.full((len(sizes), max(sizes)), -1, np.int32)
+    for r, t in enumerate(tables):
+        table[r, :len(t)] = t
+    out = B.moe_sig_request_counts(sig, dev(table), dev(np.array(sizes, np.int32)))
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.int64)
+    for r, t in enumerate(tables):
+        valid = [b for b in t if 0 <= b < nb]
+        assert np.array_equal(got[r], SO.request_counts(ref, valid)), (r, len(t))
+
+
 def test_empty_calls_are_no_ops():
     G.say("case: signature calls with nothing to do")
     c = Cache(4, 2, 16)
