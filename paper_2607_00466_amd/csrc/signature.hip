@@ -3,11 +3,14 @@
 // and per-request sums over a block table.
 //
 // capture: one thread per (layer, token, pick).  Four int8 cells share one
-// 32-bit word, so a pick adds 1 << (8 * (cell % 4)) to its word with a 32-bit
-// device atomic.  A cell never exceeds 127 (a block holds at most 127 tokens
-// and a token picks an expert at most once per layer), so no carry crosses
-// into the neighbouring cell; integer atomics make the result independent of
-// the order of the picks.
+// 32-bit word, so a pick adds 1 << (8 * (cell % 4)) to its word.  A cell
+// never exceeds 127 (a block holds at most 127 tokens and a token picks an
+// expert at most once per layer), so no carry crosses into the neighbouring
+// cell.  A workgroup first sums its picks' increments per word in an LDS hash
+// table (its 256 picks are a few tokens of one or two blocks, and popular
+// experts repeat), then adds each word's sum with one 32-bit device atomic.
+// Integer addition makes the result independent of the order and grouping
+// of the picks.
 //
 // request counts: a workgroup per (request, 1 KB stretch of the [L, E] row).
 // Its four waves split the request's blocks, 16 at a time a wave; a lane
@@ -21,10 +24,22 @@ namespace eldr {
 
 constexpr int kSigThreads = 256;
 
+// LDS hash slots of the capture: twice the most distinct words a workgroup
+// can touch (one a pick), so a probe always finds its word or a free slot.
+constexpr int kCapSlots = 2 * kSigThreads;
+constexpr uint64_t kCapFree = ~0ull;
+
 __global__ __launch_bounds__(kSigThreads) void sig_capture_kernel(
     const int32_t* __restrict__ ids, const int32_t* __restrict__ token_block, int64_t picks,
     int T, int K, int layer0, int L, int E, int num_blocks, uint32_t* __restrict__ sig_words,
     int32_t* __restrict__ rejected) {
+  __shared__ uint64_t key[kCapSlots];  // word index, or kCapFree
+  __shared__ uint32_t sum[kCapSlots];  // summed increments of the word
+  for (int i = threadIdx.x; i < kCapSlots; i += kSigThreads) {
+    key[i] = kCapFree;
+    sum[i] = 0u;
+  }
+  __syncthreads();
   const int64_t p = (int64_t)blockIdx.x * kSigThreads + threadIdx.x;  // (l * T + t) * K + j
   bool bad = false;
   if (p < picks) {
@@ -38,7 +53,19 @@ __global__ __launch_bounds__(kSigThreads) void sig_capture_kernel(
         bad = true;
       } else {
         const int64_t cell = ((int64_t)b * L + layer0 + l) * E + e;
-        atomicAdd(&sig_words[cell >> 2], 1u << (8 * (int)(cell & 3)));
+        const uint64_t word = (uint64_t)(cell >> 2);
+        const uint32_t inc = 1u << (8 * (int)(cell & 3));
+        // linear probing from a multiplicative hash of the word
+        uint32_t h = ((uint32_t)word ^ (uint32_t)(word >> 32)) * 0x9e3779b1u >> 23;
+        for (int probe = 0; probe < kCapSlots; ++probe) {
+          const uint64_t k = atomicCAS(reinterpret_cast<unsigned long long*>(&key[h]),
+                                       (unsigned long long)kCapFree, (unsigned long long)word);
+          if (k == kCapFree || k == word) {
+            atomicAdd(&sum[h], inc);
+            break;
+          }
+          h = (h + 1) & (kCapSlots - 1);
+        }
       }
     }
   }
@@ -46,6 +73,11 @@ __global__ __launch_bounds__(kSigThreads) void sig_capture_kernel(
     // one atomic per wave that saw a rejected pick
     const uint64_t m = __ballot(bad);
     if (m && (threadIdx.x % kWave) == 0) atomicAdd(rejected, (int)__popcll(m));
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kCapSlots; i += kSigThreads) {
+    const uint64_t w = key[i];
+    if (w != kCapFree) atomicAdd(&sig_words[w], sum[i]);
   }
 }
 
