@@ -29,6 +29,13 @@ MOE_ERR_UNSUPPORTED = -2
 MOE_ERR_WORKSPACE = -3
 MOE_ERR_HIP = -4
 
+# Shape limits of the layer calls (include/eldr_moe.h).
+MOE_MAX_E = 256
+MOE_MAX_K = 16
+MOE_MAX_T = 4096
+MOE_MAX_H = 16384
+MOE_MAX_I = 16384
+
 
 class MoeDims(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("E", ctypes.c_int32),

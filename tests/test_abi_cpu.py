@@ -1,6 +1,7 @@
 """The C-ABI library loads, exports what its header declares, and rejects bad
 arguments on the host before anything is launched (no GPU needed)."""
 import ctypes
+import re
 
 import pytest
 
@@ -31,6 +32,13 @@ def test_status_strings(lib):
     for st in (B.MOE_OK, B.MOE_ERR_INVALID, B.MOE_ERR_UNSUPPORTED, B.MOE_ERR_WORKSPACE, B.MOE_ERR_HIP):
         assert B.status_string(st).startswith("MOE_")
     assert B.status_string(12345) == "unknown status"
+
+
+def test_limits_match_the_header():
+    text = open(B.HEADER_PATH).read()
+    for name in ("MOE_MAX_E", "MOE_MAX_K", "MOE_MAX_T", "MOE_MAX_H", "MOE_MAX_I"):
+        m = re.search(rf"#define {name} (\d+)", text)
+        assert m and int(m.group(1)) == getattr(B, name), name
 
 
 def test_workspace_bytes(lib):

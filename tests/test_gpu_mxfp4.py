@@ -224,6 +224,18 @@ def test_mxfp4_large_batch_dealing_boundary(n):
     _check_layer(layer, g, routing=(ids, w))
 
 
+@pytest.mark.parametrize("H,I,T", [(B.MOE_MAX_H, 256, 24), (256, B.MOE_MAX_I, 80)])
+def test_mxfp4_largest_hidden_and_intermediate(H, I, T):
+    # The limits on H and I with MXFP4 experts: 256 ring slots a reduction.
+    sh = synth.LayerShape("mx_max_hi", E=4, K=2, H=H, I=I)
+    G.say(f"case: MXFP4 E=4 top-2 H={H} I={I} T={T}, expert 1 takes every token")
+    ids, w = G.fixed_bucket_routing(T, sh.E, sh.K, [(1, T)], seed=T)
+    layer = MxLayer(sh, T, seed=(H + I) % 1000)
+    g = layer.run((ids, w))
+    assert int(g["counts"][1]) == T
+    _check_layer(layer, g, routing=(ids, w))
+
+
 def test_mxfp4_empty_batch_and_invalid_routing():
     G.say("case: MXFP4 empty batch, then a duplicated id (invalid routing)")
     sh = synth.LayerShape("mx_edge", E=8, K=2, H=128, I=64)

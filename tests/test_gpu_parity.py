@@ -306,6 +306,33 @@ def test_bucket_large_batch(T, E):
     G.compare_buckets(G.fetch(buf, d), ids.astype(np.int64), E)
 
 
+@pytest.mark.parametrize("H,I,T", [(B.MOE_MAX_H, 256, 24), (256, B.MOE_MAX_I, 24),
+                                   (B.MOE_MAX_H, 256, 80), (256, B.MOE_MAX_I, 80)])
+def test_largest_hidden_and_intermediate(H, I, T):
+    # The limits on H and I: 512-step reductions and 128 or 256 row bands an
+    # expert, through the routed launch (T <= 64) and the large-batch kernels
+    # (T > 64, one bucket of 80 tokens in a 128-token pass).
+    sh = synth.LayerShape("max_hi", E=4, K=2, H=H, I=I)
+    G.say(f"case: E=4 top-2 H={H} I={I} T={T}, expert 1 takes every token")
+    layer = G.Layer(sh, T, seed=(H + I + T) % 1000)
+    ids, w = G.fixed_bucket_routing(T, sh.E, sh.K, [(1, T)], seed=T)
+    g = layer.run(routing=(ids, w))
+    assert int(g["counts"][1]) == T
+    _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
+
+
+def test_largest_batch_gate_routed():
+    # The limit on T: 4096 tokens x top-8, gate-routed end to end (buckets of
+    # about 256 tokens, two or more 128-token groups each).
+    sh = synth.LayerShape("max_t", E=128, K=8, H=256, I=128)
+    T = B.MOE_MAX_T
+    G.say(f"case: E=128 top-8 H=256 I=128 T={T}, gate-routed")
+    layer = G.Layer(sh, T, seed=3)
+    g = layer.run()
+    assert int(g["counts"].max()) > 128
+    _full_check(layer, g, True)
+
+
 def test_union_dispatch_order_at_tile_boundaries():
     # One pick per token, so each expert's count is set exactly: 15, 16 and 17
     # tokens straddle the first 16-token tile, 32/33 the second, 48/49 the
