@@ -73,7 +73,7 @@ namespace eldr {
 #define ELDR_FFN_FP4_RING 8
 #endif
 #ifndef ELDR_FFN_FP4_CHUNK
-#define ELDR_FFN_FP4_CHUNK 8
+#define ELDR_FFN_FP4_CHUNK 4
 #endif
 #ifndef ELDR_FFN_FP4_MAX_CHUNK
 #define ELDR_FFN_FP4_MAX_CHUNK 16
@@ -99,12 +99,14 @@ __host__ __device__ constexpr int slot_steps() {
   return FMT == kBf16 ? 1 : 2;
 }
 
-// Token tiles of 16 per item: at most 128 tokens of an expert for bf16 (64
-// for MXFP4); a larger bucket takes more token groups, served from L2.
+// Token tiles of 16 per item: at most 128 tokens of an expert for bf16 (32
+// for MXFP4 in batches over 64 tokens, so that the large-batch MXFP4 kernel
+// fits four workgroups a CU); a larger bucket takes more token groups,
+// served from L2.
 template <int FMT>
 __host__ __device__ constexpr int max_tiles() {
 #ifndef ELDR_FFN_FP4_MAX_TILES
-#define ELDR_FFN_FP4_MAX_TILES 4
+#define ELDR_FFN_FP4_MAX_TILES 2
 #endif
   return FMT == kBf16 ? 8 : ELDR_FFN_FP4_MAX_TILES;
 }
@@ -126,10 +128,12 @@ __host__ __device__ constexpr int ring_depth() {
 #ifndef ELDR_FFN_CYCLES2
 #define ELDR_FFN_CYCLES2 1
 #endif
-// MXFP4 moves a quarter of bf16's bytes per k-step, so it needs longer
-// chunks for the same bytes in flight, in the same 33 KB buffer: 16 token
-// rows of 16 k-steps, 32 of 8, or 64 of 4 (a pass with fewer tiles than its
-// kernel lengthens its chunks, up to 16 k-steps).
+// MXFP4 moves a quarter of bf16's bytes per k-step; its chunks fill a 17 KB
+// buffer: 16 token rows of 8 k-steps, 32 of 4, or 64 of 2 (a pass with fewer
+// tiles than its kernel lengthens its chunks, up to 16 k-steps).  Half the
+// LDS of bf16's chunks, so that more MXFP4 workgroups share a CU and cover
+// each other's item starts: measured, more workgroups a CU beat longer
+// chunks and deeper rings for these short items.
 template <int FMT, int NT>
 __host__ __device__ constexpr int chunk_steps() {
   return FMT == kMxfp4
@@ -844,8 +848,11 @@ __device__ __forceinline__ int route_tokens(const FfnArgs& a, const RouteLds& R,
 }
 
 template <int MODE, int NT, bool MULTI, int FMT, bool ROUTED>
-// (128-token passes: held to two waves a SIMD, the LDS limit, so registers never lower it)
-__global__ __launch_bounds__((ffn_threads<MODE, FMT>())) __attribute__((amdgpu_waves_per_eu(NT == 8 ? 2 : 1)))
+// (128-token passes: held to two waves a SIMD, the LDS limit, so registers
+// never lower it; the large-batch MXFP4 kernel: at least three, so that its
+// registers leave room for three or four workgroups a CU)
+__global__ __launch_bounds__((ffn_threads<MODE, FMT>()))
+__attribute__((amdgpu_waves_per_eu(NT == 8 ? 2 : (FMT == kMxfp4 && MULTI ? 3 : 1))))
 void ffn_kernel(FfnArgs a) {
   constexpr int kGroupTokens = NT * 16;  // tokens of one expert one workgroup item takes
   __shared__ __attribute__((aligned(16))) FfnLds<FMT, NT> L;

@@ -210,10 +210,11 @@ def test_mxfp4_big_buckets_take_token_groups():
     _check_layer(layer, g, (ids, w))
 
 
-@pytest.mark.parametrize("n", [64, 65])
+@pytest.mark.parametrize("n", [32, 33, 64, 65])
 def test_mxfp4_large_batch_dealing_boundary(n):
     # Batches over 64 tokens deal whole experts while every bucket fits one
-    # 64-token MXFP4 group, and (expert, band) units once one does not.
+    # 32-token MXFP4 group, and (expert, band) units once one does not (33:
+    # two groups; 64/65: two and three).
     sh = synth.LayerShape("mx_dealing", E=16, K=4, H=256, I=192)
     T = 80
     G.say(f"case: MXFP4 E=16 top-4 H=256 I=192 T={T}, expert 5 takes {n} tokens")
