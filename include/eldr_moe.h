@@ -167,10 +167,11 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * For every u < union_size, with e = union_ids[u] and its slots
  * s in [offsets[e], offsets[e+1]) holding token t = perm_token[s]:
  *   y_perm[s, :] = W2_e (silu(W1_e x[t]) * (W3_e x[t]))
- * Each active expert's weights are streamed from HBM once per call when it
- * has at most 64 tokens; a bigger bucket is split into groups of 64 tokens
- * whose workgroups run side by side on one XCD and share that XCD's L2 for
- * the repeated weight reads.  Experts outside the union are never touched.
+ * Each active expert's weights are streamed from HBM once per call when its
+ * bucket fits one token group: the whole batch when T <= 64, else 128
+ * tokens; a bigger bucket is split into groups of 128 tokens whose
+ * workgroups run side by side on one XCD and share that XCD's L2 for the
+ * repeated weight reads.  Experts outside the union are never touched.
  * Work follows the union's dispatch order (largest buckets first): with
  * T <= 64 experts are dealt round-robin over the 8 XCDs, with T > 64 their
  * (expert, row band) units are, so skewed buckets still load the XCDs evenly.
@@ -346,8 +347,9 @@ int moe_pack_mxfp4_down(const uint8_t* w2_codes, const uint8_t* w2_scales, int32
  * registers (exact: an E2M1 value times a power of two in range is a bf16
  * number) and multiplied exactly as in moe_expert_ffn, so the result equals
  * moe_expert_ffn's on the dequantized weights.  Each active expert's codes
- * and scales are streamed once per call when it has at most 64 tokens; a
- * bigger bucket is split into groups of 64 tokens sharing the XCD's L2.
+ * and scales are streamed once per call when its bucket fits one token group
+ * (the whole batch when T <= 64, else 32 tokens); a bigger bucket is split
+ * into groups of 32 tokens sharing the XCD's L2.
  * Other arguments, the workspace (moe_ffn_workspace_bytes) and the error
  * behaviour are those of moe_expert_ffn; in addition H % 64 == 0 and
  * I % 64 == 0 (else MOE_ERR_UNSUPPORTED), and the scale pointers must be
