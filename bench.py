@@ -294,6 +294,35 @@ class MxBench(Bench):
         B.moe_combine(b.y_perm, b.pair_pos, w, d, b.out)
 
 
+def mxfp4_point(steps: int, warmup: int) -> dict:
+    """The gpt-oss-120b-shaped layer (E=128, top-4, H=I=2880) at T=256 with
+    MXFP4 experts, gate-routed: the MXFP4 widening's figures for the bench
+    line (layer and up-kernel time, GB/s and fraction of HBM peak)."""
+    shape = synth.SHAPES["gpt_oss_120b"]
+    T = 256
+    log("gpt-oss MXFP4 layer for the bench line: building (synthetic weights, quantized to MXFP4)")
+    bench = MxBench(shape, T)
+    bench.step(0)
+    U = bench.union()
+    bench.rotate(U * 3 * mx_matrix_bytes(shape))
+    r = bench.time(steps, warmup)
+    lb = mx_layer_bytes(shape, T, U, True)
+    ub = mx_up_bytes(shape, T, U)
+    rec = {"workload": "gpt_oss_120b moe layer, T=256, gate-routed, MXFP4 experts", "U": U,
+           "layer_us": round(r["layer_ms"] * 1e3, 2), "ffn_up_us": round(r["up_ms"] * 1e3, 2),
+           "ffn_down_us": round(r["down_ms"] * 1e3, 2),
+           "layer_GBps": round(lb / r["layer_ms"] / 1e6, 1),
+           "layer_frac_of_hbm_peak": round(lb / r["layer_ms"] / 1e6 / HBM_PEAK_GBS, 4),
+           "ffn_up_GBps": round(ub / r["up_ms"] / 1e6, 1),
+           "ffn_up_frac_of_hbm_peak": round(ub / r["up_ms"] / 1e6 / HBM_PEAK_GBS, 4),
+           "weight_copies": len(bench.weights)}
+    log(f"gpt-oss MXFP4 gate-routed: U={U} layer {rec['layer_us']:.1f} us, up {rec['ffn_up_us']:.1f} us "
+        f"({rec['ffn_up_GBps']:.0f} GB/s)")
+    del bench
+    torch.cuda.empty_cache()
+    return rec
+
+
 def mxfp4_workload(path: str, steps: int, warmup: int, layers: int = 36,
                    cases=(None, 32, 128), formats=("mxfp4", "bf16")) -> None:
     """One gpt-oss-120b-shaped layer (E=128, top-4, H=I=2880), T=256, with MXFP4
@@ -886,6 +915,8 @@ def main() -> int:
                     help="also write the union and batch sweeps (which the bench line carries) to this file")
     ap.add_argument("--no-sweep", action="store_true",
                     help="leave the union and batch sweeps out of the bench line")
+    ap.add_argument("--no-mxfp4-line", action="store_true",
+                    help="leave the gate-routed gpt-oss MXFP4 layer out of the bench line")
     ap.add_argument("--point", action="append", default=[],
                     help="T:U -- time only this controlled-union point (repeatable; no bench line)")
     ap.add_argument("--signature", default="",
@@ -1009,6 +1040,8 @@ def main() -> int:
     if not args.no_sweep:
         log("union and batch sweeps (controlled routing) ...")
         out["sweep"] = sweep(max(20, args.steps // 2), args.warmup, args.sweep)
+    if not args.no_mxfp4_line:
+        out["mxfp4_gpt_oss"] = mxfp4_point(max(20, args.steps // 4), args.warmup)
     if args.signature:
         signature_workload(args.signature)
     if args.routing:
