@@ -90,8 +90,9 @@ int moe_abi_version(void);
  * x [T, H] fp32, w_gate [E, H] fp32 (inputs).  logits [T, E] fp32,
  * topk_ids [T, K] int32, topk_w [T, K] fp32 (outputs, all written).
  * Every expert's score is reduced in the same order, so experts with
- * identical gate rows tie exactly and the lower id wins.  Inputs must be
- * finite.
+ * identical gate rows tie exactly and the lower id wins; that order depends
+ * on H alone, so a token's logits, ids and weights are the same bits in any
+ * batch.  Inputs must be finite.
  */
 int moe_gate_topk(const float* x, const float* w_gate, moe_dims d, float* logits,
                   int32_t* topk_ids, float* topk_w, void* stream);

@@ -233,6 +233,36 @@ def test_duplicate_gate_rows_tie_to_lower_id():
     _full_check(layer, g, True)
 
 
+def _gate(x: np.ndarray, wg: torch.Tensor, shape) -> tuple:
+    T = x.shape[0]
+    d = B.dims(T, shape.H, shape.E, shape.K, shape.I)
+    logits = torch.empty((T, shape.E), device="cuda")
+    ids = torch.empty((T, shape.K), dtype=torch.int32, device="cuda")
+    wts = torch.empty((T, shape.K), device="cuda")
+    B.moe_gate_topk(torch.from_numpy(x).cuda(), wg, d, logits, ids, wts)
+    torch.cuda.synchronize()
+    return logits.cpu().numpy(), ids.cpu().numpy(), wts.cpu().numpy()
+
+
+@pytest.mark.parametrize("shape", [QWEN, GPTOSS], ids=lambda s: s.name)
+def test_gate_scores_do_not_depend_on_the_batch(shape):
+    """A token's logits, picks and weights are the same bits in any batch: the
+    batch decides the tile shape of the score kernel (4 x 4 up to 128 tokens,
+    8 x 8 above), not the reduction order of a score."""
+    G.say(f"case: gate of a 640-token batch vs sub-batches of 1..129 tokens, {shape.name}")
+    x = synth.hidden_states(640, shape.H, seed=21)
+    wg_np = synth.gate_weights(shape, seed=21)
+    wg_np[11] = wg_np[3]  # an exact tie inside the 8 x 8 tiles too
+    wg = torch.from_numpy(wg_np).cuda()
+    full = _gate(x, wg, shape)
+    assert np.array_equal(full[0][:, 3], full[0][:, 11])
+    for t0, t1 in [(0, 1), (0, 8), (5, 69), (100, 228), (200, 329), (3, 640)]:
+        part = _gate(x[t0:t1], wg, shape)
+        for name, a, b in zip(("logits", "ids", "weights"), full, part):
+            assert np.array_equal(a[t0:t1], b), f"{name} of tokens {t0}..{t1 - 1} differ"
+    G.check_gate({"logits": full[0], "ids": full[1], "weights": full[2]}, x, wg_np, shape.K)
+
+
 def test_zero_input():
     G.say("case: x = 0 (all logits 0): ids 0..K-1, weights 1/K, output 0")
     layer = G.Layer(TINY, 8)
