@@ -189,7 +189,10 @@ size_t moe_ffn_workspace_bytes(moe_dims d);
  * moe_ffn_workspace_bytes(d) bytes, 16-byte aligned, contents irrelevant.
  * Arithmetic: bf16 weights times activations carried as a pair of bf16
  * values (high part and rounded remainder, about 16 significant bits) on
- * MFMA with fp32 accumulation.
+ * MFMA with fp32 accumulation.  Every pass shape accumulates a slot's
+ * products in the same k order, so y_perm[s, :] depends on its token's x
+ * and its expert's weights alone: the same bits whatever else is in the
+ * batch (and likewise for the MXFP4, routed and fused forms).
  */
 int moe_expert_ffn(const float* x, const uint16_t* w13, const uint16_t* w2,
                    const int32_t* offsets, const int32_t* perm_token, const int32_t* union_ids,

@@ -237,6 +237,28 @@ def test_mxfp4_largest_hidden_and_intermediate(H, I, T):
     _check_layer(layer, g, routing=(ids, w))
 
 
+@pytest.mark.parametrize("path", B.FFN_PATHS)
+def test_mxfp4_layer_output_does_not_depend_on_the_batch(path):
+    """As for bf16 experts: a token's layer output is the same bits in any batch,
+    on both sides of the 64-token kernel switch and of the 32-token group."""
+    sh = synth.LayerShape("mx_batch", E=32, K=4, H=512, I=384)
+    G.say(f"case: MXFP4 E=32 top-4 H=512 I=384, 256-token batch vs sub-batches, path {path}")
+    layer = MxLayer(sh, 256, seed=24)
+    d = layer.d
+    B.moe_layer_mxfp4(layer.x, layer.wg, layer.up, layer.down, d, layer.buf, path=path)
+    torch.cuda.synchronize()
+    full = G.fetch(layer.buf, d)
+    for t0, t1 in [(0, 1), (0, 16), (16, 80), (100, 164), (0, 65), (80, 209), (3, 256)]:
+        ds = B.dims(t1 - t0, sh.H, sh.E, sh.K, sh.I)
+        buf = B.LayerBuffers.allocate(ds)
+        B.moe_layer_mxfp4(layer.x[t0:t1].contiguous(), layer.wg, layer.up, layer.down, ds, buf,
+                          path=path)
+        torch.cuda.synchronize()
+        part = G.fetch(buf, ds)
+        for k in ("ids", "weights", "out"):
+            assert np.array_equal(full[k][t0:t1], part[k]), f"{k} of tokens {t0}..{t1 - 1} differ"
+
+
 def test_mxfp4_empty_batch_and_invalid_routing():
     G.say("case: MXFP4 empty batch, then a duplicated id (invalid routing)")
     sh = synth.LayerShape("mx_edge", E=8, K=2, H=128, I=64)

@@ -263,6 +263,24 @@ def test_gate_scores_do_not_depend_on_the_batch(shape):
     G.check_gate({"logits": full[0], "ids": full[1], "weights": full[2]}, x, wg_np, shape.K)
 
 
+@pytest.mark.parametrize("path", B.FFN_PATHS)
+def test_layer_output_does_not_depend_on_the_batch(path):
+    """A token's gate output and layer output are the same bits whatever else is
+    in its batch: sub-batches on both sides of the 64-token kernel switch and
+    of the 128-token group give the rows of the full batch's result."""
+    G.say(f"case: qwen layer, 256-token batch vs sub-batches of 1..253 tokens, path {path}")
+    layer = G.Layer(QWEN, 256, seed=23, experts_on_host=False)
+    full = layer.run(path=path)
+    for t0, t1 in [(0, 1), (0, 16), (16, 80), (100, 164), (0, 65), (80, 209), (3, 256)]:
+        d = B.dims(t1 - t0, QWEN.H, QWEN.E, QWEN.K, QWEN.I)
+        buf = B.LayerBuffers.allocate(d)
+        B.moe_layer(layer.x[t0:t1].contiguous(), layer.wg, layer.p13, layer.p2, d, buf, path=path)
+        torch.cuda.synchronize()
+        part = G.fetch(buf, d)
+        for k in ("logits", "ids", "weights", "out"):
+            assert np.array_equal(full[k][t0:t1], part[k]), f"{k} of tokens {t0}..{t1 - 1} differ"
+
+
 def test_zero_input():
     G.say("case: x = 0 (all logits 0): ids 0..K-1, weights 1/K, output 0")
     layer = G.Layer(TINY, 8)
