@@ -283,30 +283,33 @@ def gpt_oss_mx():
     return MxLayer(GPTOSS, 256)
 
 
-def _sampled(layer: MxLayer, g: dict, ids, wts, sample, label):
-    experts = sorted(set(np.asarray(ids)[sample].ravel().tolist()))
-    q = layer.host_q(experts)
-    sub = MX.moe_layer_routed(layer.x_np[sample], np.asarray(ids)[sample],
-                              np.asarray(wts, np.float64)[sample], q["w1"], q["w3"], q["w2"], GPTOSS.E)
-    G.check_output(g["out"][sample], sub["out"], label)
+def _every_row(layer: MxLayer, g: dict, ids, wts, label):
+    """Every slot row and every output row against the oracle on the given
+    routing (the oracle dequantizes each union expert's matrices once)."""
+    ids = np.asarray(ids, np.int64)
+    q = layer.host_q(sorted(set(ids.ravel().tolist())))
+    ref = MX.moe_layer_routed(layer.x_np, ids, np.asarray(wts, np.float64), q["w1"], q["w3"],
+                              q["w2"], GPTOSS.E)
+    G.check_output(g["y_slots"], ref["y_slots"], f"every slot, {label}")
+    G.check_output(g["out"], ref["out"], f"every token, {label}")
 
 
-def test_gpt_oss_mxfp4_gate_routed_sampled(gpt_oss_mx):
-    G.say("case: gpt-oss MXFP4 layer T=256, gate-routed, sampled tokens")
+def test_gpt_oss_mxfp4_gate_routed(gpt_oss_mx):
+    G.say("case: gpt-oss MXFP4 layer T=256, gate-routed, all tokens and slots")
     g = gpt_oss_mx.run()
     G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
     near = G.check_gate(g, gpt_oss_mx.x_np, gpt_oss_mx.wg_np, GPTOSS.K)
     ids = g["ids"].astype(np.int64)
     G.compare_buckets(g, ids, GPTOSS.E)
-    sample = [t for t in (0, 93, 200, 255) if not near[t]]
-    _sampled(gpt_oss_mx, g, ids, g["weights"], sample, "sampled tokens")
+    # on the GPU's own routing, whose near-tie picks check_gate has validated
+    _every_row(gpt_oss_mx, g, ids, g["weights"], f"gate-routed ({int(near.sum())} near-ties)")
 
 
 @pytest.mark.parametrize("U", [32, 128])
-def test_gpt_oss_mxfp4_controlled_union_sampled(gpt_oss_mx, U):
-    G.say(f"case: gpt-oss MXFP4 layer T=256, controlled union U={U}, sampled tokens")
+def test_gpt_oss_mxfp4_controlled_union(gpt_oss_mx, U):
+    G.say(f"case: gpt-oss MXFP4 layer T=256, controlled union U={U}, all tokens and slots")
     ids, w, _ = synth.controlled_routing(256, GPTOSS.E, GPTOSS.K, U=U, seed=U)
     g = gpt_oss_mx.run((ids, w))
     G.compare_buckets(g, ids, GPTOSS.E)
     G.say(f"  union size {g['union_size']}, max bucket {g['counts'].max()}")
-    _sampled(gpt_oss_mx, g, ids, w, [3, 130, 254], f"sampled tokens, U={U}")
+    _every_row(gpt_oss_mx, g, ids, w, f"U={U}")
