@@ -951,7 +951,7 @@ def main() -> int:
     args = ap.parse_args()
     FFN_PATH = args.ffn_path
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+        print(f"bench.py measures one GPU: the layer runs on one GPU and has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         return 2
     if not torch.cuda.is_available():
