@@ -178,11 +178,14 @@ def test_large_batch_dealing_boundary(n):
     _full_check(layer, g, False, routing=(ids.astype(np.int64), w))
 
 
-def test_ragged_shape_partial_bands():
-    # H and I multiples of 32 but not of the 64/128-row bands; E not a multiple of 8.
-    G.say("case: ragged shape E=13 top-3 H=352 I=96 T=21")
+@pytest.mark.parametrize("T", [21, 203])
+def test_ragged_shape_partial_bands(T):
+    # H and I multiples of 32 but not of the 64/128-row bands; E not a multiple of
+    # 8.  T = 203 takes the large-batch kernels and the gate's 8 x 8 tiles, with a
+    # partial last tile of experts and of tokens.
+    G.say(f"case: ragged shape E=13 top-3 H=352 I=96 T={T}")
     shape = synth.LayerShape("ragged", E=13, K=3, H=352, I=96)
-    layer = G.Layer(shape, 21, seed=4)
+    layer = G.Layer(shape, T, seed=4)
     _full_check(layer, layer.run(), True)
 
 
@@ -204,10 +207,11 @@ def test_k_equals_e():
     _full_check(layer, g, True)
 
 
-@pytest.mark.parametrize("T", [5, 70])
+@pytest.mark.parametrize("T", [5, 70, 200])
 def test_single_expert(T):
     # E = K = 1: every token on expert 0 with weight 1, a union of one.  T = 70
-    # takes the large-batch kernels with one 128-token group.
+    # takes the large-batch kernels with one 128-token group; T = 200 two groups,
+    # and the gate's 8 x 8 tiles with one live expert each.
     G.say(f"case: E=1 top-1 H=256 I=128 T={T}, gate-routed")
     shape = synth.LayerShape("single_expert", E=1, K=1, H=256, I=128)
     layer = G.Layer(shape, T, seed=40 + T)
